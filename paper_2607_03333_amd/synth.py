@@ -1,0 +1,350 @@
+"""Seeded synthetic workloads for the forked-decode hot path.
+
+This module only draws numbers and lays out a scenario; it holds none of the
+method's arithmetic (no attention, no argmax, no accept, no block allocation).
+The product path, the tests and the oracle all take their inputs from here.
+
+The paper measures on agent benchmarks with Qwen3 models served by vLLM
+(Section 6.1); neither the benchmarks nor the weights are available, so seeded
+Gaussian data with the workload's structure stands in for them:
+
+* one shared prefix per session (the system + user + history prompt that D1's
+  fork reuses, Section 4.1; about 15K tokens of context in the paper's
+  measurement of probe cost);
+* a main thread plus forked probes per session, each with a private suffix
+  (the chain of thought between the fork and the tool call is about 2,000
+  tokens, Section 1);
+* verify threads that carry ``K`` draft rows (the rejected probe's tool-call
+  body, Section 4.3) and greedy logits whose argmax is planted by construction:
+  every row has a value above all others at a chosen index, sometimes at two
+  indices (a tie), so the greedy token and the expected accepted length are
+  known without computing an argmax.
+
+Seeds (42 is the seed the paper uses for every call, Section 6.1): the
+workload stream ``numpy.random.default_rng([42, index])`` draws, in order, the
+suffix lengths, the pool free order, per-step Q, then per verify step the
+planted greedy tokens and ties, match counts and drafts. Bulk arrays come from
+their own streams so they can be drawn in parallel: session ``s``'s prefix K
+then V from ``[42, index, 1, s]``, sequence ``t``'s private K then V from
+``[42, index, 2, t]``, verify step ``j``'s raw logits from ``[42, index, 3, j]``.
+"""
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+from dataclasses import dataclass, field
+import math
+
+import numpy as np
+
+F32 = "f32"
+BF16 = "bf16"
+
+# The five workloads of the benchmark, by what they are (sizes stated in full).
+CONFIGS = [
+    dict(name="tiny-fork-f32", hq=4, hkv=2, d=64, block_size=16, dtype=F32,
+         sessions=1, probes=1, prefix=256, suffix=("fixed", [32, 8]),
+         verify_k=4, vocab=512, logits_dtype=F32, planted_n="fixed2",
+         q_scale_in_softmax=0.125, layout="decode-then-verify"),
+    dict(name="qwen3-4b-decode", hq=32, hkv=8, d=128, block_size=16, dtype=BF16,
+         sessions=8, probes=1, prefix=4096, suffix=("uniform", 1, 2048),
+         verify_k=0, vocab=0, logits_dtype=BF16, layout="decode"),
+    dict(name="qwen3-32b-decode", hq=64, hkv=8, d=128, block_size=16, dtype=BF16,
+         sessions=16, probes=4, prefix=16384, suffix=("uniform", 1, 2000),
+         verify_k=0, vocab=0, logits_dtype=BF16, layout="decode"),
+    dict(name="qwen3-32b-verify", hq=64, hkv=8, d=128, block_size=16, dtype=BF16,
+         sessions=16, probes=0, prefix=16384, suffix=("fixed", [0]),
+         verify_k=16, vocab=151936, logits_dtype=BF16, planted_n="geom0.3",
+         layout="verify"),
+    dict(name="qwen3-30b-a3b-mixed", hq=32, hkv=4, d=128, block_size=16, dtype=BF16,
+         sessions=64, probes=2, prefix=32768, suffix=("loguniform", 1, 4096),
+         verify_k=8, vocab=151936, logits_dtype=BF16, planted_n="geom0.3",
+         layout="mixed"),
+]
+
+PLANT_VALUE = 7.0     # planted greedy logit; every other logit is clipped to [-6, 6]
+CLIP = 6.0
+TIE_PROB = 0.25       # chance that a row carries a second planted maximum
+
+
+def config_index(name_or_index):
+    if isinstance(name_or_index, int):
+        return name_or_index
+    for i, c in enumerate(CONFIGS):
+        if c["name"] == name_or_index:
+            return i
+    raise KeyError(name_or_index)
+
+
+# --- storage conversions (exact bit operations, no rounding choices beyond RNE) ---
+def f32_to_bf16_bits(x):
+    """Round float32 to bfloat16 (round to nearest, ties to even); returns uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounding = ((u >> 16) & 1) + np.uint32(0x7FFF)
+    return ((u + rounding) >> 16).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b):
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def to_storage(x, dtype):
+    return f32_to_bf16_bits(x) if dtype == BF16 else np.ascontiguousarray(x, dtype=np.float32)
+
+
+def to_f64(x, dtype):
+    """Exact upcast of stored values to float64."""
+    if dtype == BF16:
+        return bf16_bits_to_f32(x).astype(np.float64)
+    return np.asarray(x, dtype=np.float64)
+
+
+@dataclass
+class Thread:
+    seq: int            # sequence id (ids are issued 0, 1, 2, ... in creation order)
+    session: int
+    role: str           # "main" or "probe"
+    suffix: int         # private tokens appended after the fork (includes the decode token)
+    drafts: int = 0     # draft tokens appended before the verify step
+
+
+@dataclass
+class Step:
+    """One call of the hot path: the threads, their rows and groups, Q, and verify data."""
+    seqs: list
+    n_rows: list
+    groups: list
+    q: np.ndarray                       # [rows, Hq, D] in storage dtype
+    ops_before: list                    # scenario ops to apply before this step
+    logits: np.ndarray = None           # [S*(K+1), V] storage dtype
+    drafts: np.ndarray = None           # [S, K] int32
+    planted_greedy: np.ndarray = None   # [S*(K+1)] greedy token per row, by construction
+    planted_accept: np.ndarray = None   # [S]
+    planted_next: np.ndarray = None     # [S]
+    verify_k: int = 0
+
+
+@dataclass
+class Workload:
+    index: int
+    name: str
+    hq: int
+    hkv: int
+    d: int
+    block_size: int
+    dtype: str
+    logits_dtype: str
+    sm_scale: float
+    num_blocks: int
+    free_order: np.ndarray
+    threads: list
+    prefix_len: list                    # per session
+    prefix_k: list                      # per session [P, Hkv, D] storage dtype
+    prefix_v: list
+    suffix_k: dict                      # per seq [suffix + drafts, Hkv, D]
+    suffix_v: dict
+    steps: list = field(default_factory=list)
+
+    def context(self, seq, length=None):
+        """Logical K, V of a thread (prefix then private tokens), storage dtype."""
+        t = next(t for t in self.threads if t.seq == seq)
+        k = np.concatenate([self.prefix_k[t.session], self.suffix_k[seq]])
+        v = np.concatenate([self.prefix_v[t.session], self.suffix_v[seq]])
+        if length is not None:
+            k, v = k[:length], v[:length]
+        return k, v
+
+    def thread_len(self, seq, upto_step):
+        """Context length of ``seq`` when step ``upto_step`` runs."""
+        n = 0
+        for step in self.steps[: upto_step + 1]:
+            for op in step.ops_before:
+                if op[0] == "append" and op[1] == seq:
+                    n += op[2]
+                if op[0] == "fork" and op[2] == seq:
+                    n += self._len_at_fork(op[1], step, op)
+        return n
+
+    def _len_at_fork(self, parent, step, fork_op):
+        n = 0
+        for st in self.steps:
+            for op in st.ops_before:
+                if op is fork_op:
+                    return n
+                if op[0] == "append" and op[1] == parent:
+                    n += op[2]
+        return n
+
+    def unique_kv_bytes(self, step_index):
+        """KV bytes a step must read once: each shared prefix once, each private part once."""
+        step = self.steps[step_index]
+        elem = 4 if self.dtype == F32 else 2
+        per_tok = 2 * self.hkv * self.d * elem
+        sessions = sorted({next(t.session for t in self.threads if t.seq == s) for s in step.seqs})
+        total = sum(self.prefix_len[s] for s in sessions)
+        for s in step.seqs:
+            t = next(t for t in self.threads if t.seq == s)
+            total += self.thread_len(s, step_index) - self.prefix_len[t.session]
+        return total * per_tok
+
+
+def _draw_suffix(rng, spec, n):
+    kind = spec[0]
+    if kind == "fixed":
+        vals = list(spec[1])
+        return [vals[i % len(vals)] for i in range(n)]
+    if kind == "uniform":
+        return [int(x) for x in rng.integers(spec[1], spec[2] + 1, size=n)]
+    if kind == "loguniform":
+        lo, hi = spec[1], spec[2]
+        u = rng.uniform(0.0, math.log(hi + 1), size=n)
+        return [int(min(max(math.floor(math.exp(x)), lo), hi)) for x in u]
+    raise ValueError(kind)
+
+
+def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=None,
+         block_size=None, q_gain=1.0, tie_prob=TIE_PROB):
+    """Build workload ``index`` (0..4), optionally shrunk for fast tests.
+
+    Overrides keep the workload's structure (forks, rows, GQA, dtype) while
+    changing its size. ``q_gain`` multiplies Q (a sharper softmax).
+    """
+    index = config_index(index)
+    cfg = dict(CONFIGS[index])
+    if sessions is not None:
+        cfg["sessions"] = sessions
+    if prefix is not None:
+        cfg["prefix"] = prefix
+    if suffix is not None:
+        cfg["suffix"] = suffix
+    if vocab is not None:
+        cfg["vocab"] = vocab
+    if verify_k is not None:
+        cfg["verify_k"] = verify_k
+    if block_size is not None:
+        cfg["block_size"] = block_size
+    rng = np.random.default_rng([42, index])
+    hq, hkv, d, bs, dtype = cfg["hq"], cfg["hkv"], cfg["d"], cfg["block_size"], cfg["dtype"]
+    n_sess, n_probe, plen = cfg["sessions"], cfg["probes"], cfg["prefix"]
+    kd = cfg["verify_k"]
+    layout = cfg["layout"]
+    if "q_scale_in_softmax" in cfg:
+        sm_scale = float(np.float32(cfg["q_scale_in_softmax"]))
+    else:
+        sm_scale = float(np.float32(1.0 / math.sqrt(d)))
+
+    # Threads: mains get ids 0..S-1, probes follow in session order.
+    threads = []
+    for s in range(n_sess):
+        threads.append(Thread(seq=s, session=s, role="main", suffix=0))
+    nid = n_sess
+    for s in range(n_sess):
+        for _ in range(n_probe):
+            threads.append(Thread(seq=nid, session=s, role="probe", suffix=0))
+            nid += 1
+    by_session = {s: [t for t in threads if t.session == s] for s in range(n_sess)}
+    ordered = [t for s in range(n_sess) for t in by_session[s]]   # main, probes per session
+    lens = _draw_suffix(rng, cfg["suffix"], len(ordered))
+    for t, n in zip(ordered, lens):
+        t.suffix = n
+    verify_threads = []
+    if layout in ("verify", "mixed", "decode-then-verify"):
+        for s in range(n_sess):
+            by_session[s][0].drafts = kd
+            verify_threads.append(by_session[s][0])
+
+    blocks = sum(-(-plen // bs) for _ in range(n_sess))
+    blocks += sum(-(-(t.suffix + t.drafts) // bs) + 1 for t in threads)
+    num_blocks = blocks + 16
+    free_order = rng.permutation(num_blocks).astype(np.int32)
+
+    def normal(shape, r=rng):
+        return r.standard_normal(shape, dtype=np.float32)
+
+    def kv_pair(key, n):
+        r = np.random.default_rng([42, index] + list(key))
+        return (to_storage(normal((n, hkv, d), r), dtype),
+                to_storage(normal((n, hkv, d), r), dtype))
+
+    jobs = [((1, s), plen) for s in range(n_sess)]
+    jobs += [((2, t.seq), t.suffix + t.drafts) for t in ordered]
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
+    prefix_k = [pairs[s][0] for s in range(n_sess)]
+    prefix_v = [pairs[s][1] for s in range(n_sess)]
+    suffix_k = {t.seq: pairs[n_sess + i][0] for i, t in enumerate(ordered)}
+    suffix_v = {t.seq: pairs[n_sess + i][1] for i, t in enumerate(ordered)}
+
+    build_ops = [("new", t.seq) for t in threads if t.role == "main"]
+    build_ops += [("append", t.seq, plen) for t in threads if t.role == "main"]
+    build_ops += [("fork", by_session[t.session][0].seq, t.seq) for t in threads if t.role == "probe"]
+    build_ops += [("append", t.seq, t.suffix) for t in ordered if t.suffix > 0]
+    draft_ops = [("append", t.seq, t.drafts) for t in verify_threads if t.drafts > 0]
+
+    wl = Workload(index=index, name=cfg["name"], hq=hq, hkv=hkv, d=d, block_size=bs,
+                  dtype=dtype, logits_dtype=cfg["logits_dtype"], sm_scale=sm_scale,
+                  num_blocks=num_blocks, free_order=free_order, threads=threads,
+                  prefix_len=[plen] * n_sess, prefix_k=prefix_k, prefix_v=prefix_v,
+                  suffix_k=suffix_k, suffix_v=suffix_v)
+
+    def q_for(n_rows_total):
+        return to_storage(normal((n_rows_total, hq, d)) * np.float32(q_gain), dtype)
+
+    def decode_step(ops):
+        seqs = [t.seq for t in ordered]
+        rows = [1] * len(seqs)
+        groups = [t.session for t in ordered]
+        return Step(seqs=seqs, n_rows=rows, groups=groups, q=q_for(len(seqs)), ops_before=ops)
+
+    if layout == "decode":
+        wl.steps.append(decode_step(build_ops))
+    elif layout == "decode-then-verify":
+        wl.steps.append(decode_step(build_ops))
+        seqs = [t.seq for t in verify_threads]
+        rows = [kd + 1] * len(seqs)
+        wl.steps.append(Step(seqs=seqs, n_rows=rows, groups=[t.session for t in verify_threads],
+                             q=q_for(sum(rows)), ops_before=draft_ops, verify_k=kd))
+    elif layout == "verify":
+        seqs = [t.seq for t in verify_threads]
+        rows = [kd + 1] * len(seqs)
+        wl.steps.append(Step(seqs=seqs, n_rows=rows, groups=[t.session for t in verify_threads],
+                             q=q_for(sum(rows)), ops_before=build_ops + draft_ops, verify_k=kd))
+    elif layout == "mixed":
+        seqs = [t.seq for t in ordered]
+        rows = [kd + 1 if t.drafts else 1 for t in ordered]
+        wl.steps.append(Step(seqs=seqs, n_rows=rows, groups=[t.session for t in ordered],
+                             q=q_for(sum(rows)), ops_before=build_ops + draft_ops, verify_k=kd))
+    else:
+        raise ValueError(layout)
+
+    # Verify data: planted greedy tokens, ties, match counts and drafts.
+    for j, step in enumerate(wl.steps):
+        if step.verify_k == 0:
+            continue
+        vocab = cfg["vocab"]
+        n_ver = len(verify_threads)
+        rows = n_ver * (kd + 1)
+        raw = np.clip(normal((rows, vocab), np.random.default_rng([42, index, 3, j])), -CLIP, CLIP)
+        target = rng.integers(0, vocab, size=rows)
+        tie = rng.random(rows) < tie_prob
+        partner = (target + 1 + rng.integers(0, vocab - 1, size=rows)) % vocab
+        raw[np.arange(rows), target] = PLANT_VALUE
+        raw[np.arange(rows)[tie], partner[tie]] = PLANT_VALUE
+        greedy = np.where(tie, np.minimum(target, partner), target).astype(np.int64)
+        if cfg.get("planted_n") == "fixed2":
+            n_match = np.full(n_ver, 2, dtype=np.int64)
+        else:
+            n_match = rng.geometric(0.3, size=n_ver).astype(np.int64) - 1
+        n_match = np.minimum(n_match, kd)
+        drafts = rng.integers(0, vocab, size=(n_ver, kd)).astype(np.int64)
+        g = greedy.reshape(n_ver, kd + 1)
+        for s in range(n_ver):
+            drafts[s, : n_match[s]] = g[s, : n_match[s]]
+            if n_match[s] < kd:
+                drafts[s, n_match[s]] = (g[s, n_match[s]] + 1 + rng.integers(0, vocab - 1)) % vocab
+        step.logits = to_storage(raw, cfg["logits_dtype"])
+        step.drafts = drafts.astype(np.int32)
+        step.planted_greedy = greedy
+        step.planted_accept = n_match
+        step.planted_next = g[np.arange(n_ver), n_match]
+    return wl
