@@ -1,0 +1,229 @@
+/*
+ * spork.h -- C ABI of libspork: the forked-decode hot path of SPORK
+ * (Self-Speculative Forking, arXiv 2607.03333) on AMD MI355X (gfx950).
+ *
+ * What the library computes
+ *   - spork_fork: a probe thread forked from a main thread reuses the main
+ *     thread's prefix KV blocks in place (design D1, Section 4.1: the probe's
+ *     prefill becomes a prefix-cache hit). Blocks are shared through a
+ *     reference-counted block table and copied on first write.
+ *   - spork_attn_decode: one decode step of attention for a batch of main and
+ *     probe threads over their paged KV. Threads of one fork group share their
+ *     common prefix; its KV is streamed once per group, each thread's private
+ *     suffix once per thread, and the parts are merged by log-sum-exp.
+ *   - spork_verify_accept: the D3 step (Section 4.3): the rejected probe's
+ *     tokens enter the main thread as K draft rows with a causal rule over the
+ *     drafts; the greedy token of every verify row is the lowest index of its
+ *     row maximum, and the accepted length is the longest draft prefix that
+ *     equals the greedy tokens (decoding resumes after the first mismatch).
+ *
+ * Conventions
+ *   - Every entry point returns SPORK_OK (0) or a negative status and never
+ *     throws or aborts; spork_last_error() gives a message for the calling
+ *     thread's last failure.
+ *   - Arguments are validated before anything is launched or changed: on an
+ *     error no kernel is launched and the block manager is unchanged.
+ *   - "host" pointers are CPU memory; "device" pointers are GPU memory of the
+ *     current HIP device. All device memory is owned by the caller; launches go
+ *     on the caller's stream and the library never synchronises it. Results
+ *     are valid once that stream has been synchronised.
+ *   - Objects (spork_cache, spork_plan) are not thread-safe; callers serialise
+ *     calls on one object.
+ *
+ * KV pool layout (both pools have num_blocks blocks of block_size tokens):
+ *   K pool: [num_blocks][Hkv][block_size][D]   (token-major inside a block)
+ *   V pool: [num_blocks][Hkv][D][block_size]   (channel-major inside a block)
+ *   Token slot s lives in block s / block_size at offset s % block_size.
+ *   The channel-major V block gives the P.V matrix product its operand with
+ *   8 consecutive tokens per 16-byte load.
+ * Query / output rows: q and out are [rows][Hq][D]; thread t of a batch owns
+ *   the next n_rows[t] rows, in batch order. Row r of thread t sits at context
+ *   position L_t - n_rows[t] + r (L_t includes the rows' own tokens) and
+ *   attends to positions 0 .. L_t - n_rows[t] + r. Query head h reads KV head
+ *   h / (Hq / Hkv). lse is [rows][Hq] float32, natural log.
+ */
+#ifndef SPORK_H
+#define SPORK_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define SPORK_OK 0
+#define SPORK_E_INVAL (-1)       /* bad argument (null pointer, bad size, unknown id) */
+#define SPORK_E_NOBLOCKS (-2)    /* the free queue cannot serve an append */
+#define SPORK_E_UNSUPPORTED (-3) /* dtype / head_dim / block_size without a kernel */
+#define SPORK_E_CAPACITY (-4)    /* a caller buffer is too small; required size returned */
+#define SPORK_E_HIP (-5)         /* a HIP call or kernel launch failed */
+
+/* ---- element types ----------------------------------------------------- */
+#define SPORK_DTYPE_F32 0
+#define SPORK_DTYPE_BF16 1
+
+/* Message for the calling thread's last failure ("" if none). Static storage
+ * owned by the library, valid until the thread's next failing call. */
+const char* spork_last_error(void);
+
+/* ABI version, bumped on any incompatible change. */
+int spork_version(void);
+
+/* ======================================================================== *
+ *  Block manager (host). Section 4.1: the fork shares the parent's prefix KV.
+ * ======================================================================== */
+typedef struct spork_cache spork_cache;
+
+/* Create a block manager over num_blocks blocks of block_size tokens.
+ * free_order (host, num_blocks entries, nullable): the initial free queue, a
+ * permutation of 0..num_blocks-1 taken from the front (NULL = 0,1,2,...).
+ * Blocks freed later go to the back of the queue. *out receives the handle,
+ * owned by the caller until spork_cache_destroy. */
+int spork_cache_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,
+                       spork_cache** out);
+int spork_cache_destroy(spork_cache* cache);
+
+/* New empty sequence. Sequence ids are issued 0, 1, 2, ... in creation order
+ * (spork_seq_new and spork_fork both create) and are never reused. */
+int spork_seq_new(spork_cache* cache, int32_t* seq_out);
+
+/* Reserve slots for n_tokens new tokens at the end of seq.
+ * slots_out (host, n_tokens int64): physical slot of each new token.
+ * cow_out (host, 3 int32) / n_cow_out: when the sequence ends inside a block
+ * that another sequence also references, the first new token makes a private
+ * copy: (src_block, dst_block, n_valid) is returned and *n_cow_out = 1; the
+ * caller must copy those n_valid slots (spork_kv_copy) before writing the new
+ * tokens. Otherwise *n_cow_out = 0. New blocks come from the free queue front;
+ * a copy target is taken before any new block. SPORK_E_NOBLOCKS if the queue
+ * is too short (nothing changes). */
+int spork_seq_append(spork_cache* cache, int32_t seq, int32_t n_tokens, int64_t* slots_out,
+                     int32_t* cow_out, int32_t* n_cow_out);
+
+/* Copy-on-write fork (Section 4.1, D1): a new sequence whose table is a copy
+ * of parent's; every referenced block gains one reference; no KV is copied. */
+int spork_fork(spork_cache* cache, int32_t parent_seq, int32_t* child_seq_out);
+
+/* Drop seq: one reference per table entry in table order; blocks that reach
+ * zero references go to the back of the free queue. */
+int spork_seq_free(spork_cache* cache, int32_t seq);
+
+int spork_seq_len(const spork_cache* cache, int32_t seq, int32_t* len_out);
+
+/* Block table of seq into out (host, cap entries). *n_out = its length;
+ * SPORK_E_CAPACITY (with *n_out set) if cap is too small. */
+int spork_block_table(const spork_cache* cache, int32_t seq, int32_t* out, int32_t cap,
+                      int32_t* n_out);
+int spork_refcount(const spork_cache* cache, int32_t block, int32_t* out);
+
+/* The free queue, front first, into out (host, cap entries); same capacity rule. */
+int spork_free_blocks(const spork_cache* cache, int32_t* out, int32_t cap, int32_t* n_out);
+
+/* ======================================================================== *
+ *  Shapes and KV writes (setup work around the hot path).
+ * ======================================================================== */
+typedef struct spork_shape {
+  int32_t hq;         /* query heads */
+  int32_t hkv;        /* KV heads; hq % hkv == 0 */
+  int32_t head_dim;   /* D */
+  int32_t block_size; /* tokens per block */
+  int32_t dtype;      /* SPORK_DTYPE_*: element type of q, K/V pools and out */
+  float sm_scale;     /* softmax scale applied to q.k */
+} spork_shape;
+
+/* Write n tokens' K and V into the pools.
+ * slots (device, n int64): target slots; k_new, v_new (device, [n][Hkv][D],
+ * dtype): the values. Slots outside [0, num_blocks*block_size) are not
+ * written and are counted into *bad_slots (device int32, nullable, not
+ * cleared by the call). */
+int spork_kv_write(const spork_shape* shape, void* k_cache, void* v_cache, int32_t num_blocks,
+                   const int64_t* slots, const void* k_new, const void* v_new, int32_t n,
+                   int32_t* bad_slots, hipStream_t stream);
+
+/* The copy of copy-on-write: slots 0..n_valid-1 of block src into block dst,
+ * every head, both pools (device pools, host arguments). */
+int spork_kv_copy(const spork_shape* shape, void* k_cache, void* v_cache, int32_t num_blocks,
+                  int32_t src_block, int32_t dst_block, int32_t n_valid, hipStream_t stream);
+
+/* ======================================================================== *
+ *  Batch plan (host): the work of one decode / verify step.
+ * ======================================================================== */
+typedef struct spork_plan spork_plan;
+
+typedef struct spork_plan_info {
+  int32_t n_threads;
+  int32_t n_rows;          /* query rows (sum of n_rows) */
+  int32_t n_groups;        /* fork groups (cascade units) */
+  int32_t n_items;         /* (prefix or suffix range, KV head) work items */
+  int32_t n_waves;         /* attention workgroups launched (incl. padding) */
+  int32_t n_partials;      /* partial-result rows written by the attention kernel */
+  int32_t max_row_tiles;   /* 16-row MFMA tiles per workgroup */
+  int32_t pad_;
+  size_t image_bytes;      /* size of the device image (spork_plan_image) */
+  size_t workspace_bytes;  /* workspace spork_attn_decode needs */
+  int64_t shared_tokens;   /* prefix tokens read once per group (sum over groups) */
+  int64_t private_tokens;  /* suffix tokens read once per thread */
+  int64_t unique_kv_bytes; /* (shared + private tokens) * 2 * Hkv * D * elem */
+  int64_t flat_kv_bytes;   /* bytes a kernel without prefix sharing reads */
+} spork_plan_info;
+
+/* Plan one step for n_threads threads.
+ * seqs, n_rows, groups (host, n_threads each): the sequences, their query
+ * rows (1 for decode, K+1 for a verify thread; 1 <= n_rows <= length) and
+ * their fork group (threads with the same group id >= 0 share their longest
+ * common block-table prefix; -1 = no group). n_cu: compute units to balance
+ * for (0 = 256, one MI355X). The plan keeps no reference to the cache. */
+int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const int32_t* seqs,
+                      const int32_t* n_rows, const int32_t* groups, int32_t n_threads,
+                      int32_t n_cu, spork_plan** out);
+int spork_plan_destroy(spork_plan* plan);
+int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info);
+
+/* Copy the plan's device image (block tables, work list, merge lists) into
+ * host_dst (cap bytes, >= info.image_bytes). The caller places it in device
+ * memory (256-byte aligned) and passes that copy as dev_image below. */
+int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap);
+
+/* ======================================================================== *
+ *  Hot path.
+ * ======================================================================== */
+
+/* Batched decode attention of main and probe rows (Sections 4.1 and 4.3).
+ * q (device [rows][Hq][D] dtype); k_cache, v_cache (device pools);
+ * out (device [rows][Hq][D] dtype); lse (device [rows][Hq] float32, nullable);
+ * workspace (device, ws_bytes >= info.workspace_bytes, any contents).
+ * Kernels: cascade partial attention over prefix and suffix ranges, then the
+ * log-sum-exp merge. */
+int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void* q,
+                      const void* k_cache, const void* v_cache, void* out, float* lse,
+                      void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace for the argmax + accept part of spork_verify_accept. */
+int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t vocab,
+                                 size_t* bytes);
+
+/* D3 verify step (Section 4.3): optional attention over the plan (pass
+ * plan = NULL to run only the accept), then greedy argmax over the verify
+ * logits and the longest-prefix accept.
+ * logits (device [n_verify*(k_drafts+1)][vocab], logits_dtype): row
+ * s*(k_drafts+1)+r is verify row r of verify thread s; drafts (device
+ * [n_verify][k_drafts] int32). Outputs (device int32): accept_len[n_verify]
+ * = first r < k_drafts whose greedy token differs from the draft, else
+ * k_drafts; next_token[n_verify] = greedy token of row accept_len;
+ * argmax_out[n_verify*(k_drafts+1)] (nullable) = every row's greedy token.
+ * Ties pick the lowest vocabulary index; logits must be finite.
+ * workspace: the attention's workspace followed (at a 256-byte aligned
+ * offset) by spork_verify_workspace_bytes; ws_bytes covers both. */
+int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q,
+                        const void* k_cache, const void* v_cache, void* out, float* lse,
+                        const void* logits, int32_t logits_dtype, int32_t vocab,
+                        const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
+                        int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
+                        void* workspace, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPORK_H */

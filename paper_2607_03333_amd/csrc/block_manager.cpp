@@ -1,0 +1,78 @@
+#include "block_manager.h"
+
+namespace spork {
+
+BlockManager::BlockManager(int32_t num_blocks, int32_t block_size, const int32_t* free_order)
+    : num_blocks_(num_blocks), block_size_(block_size), ref_(num_blocks, 0) {
+  for (int32_t i = 0; i < num_blocks; ++i) free_.push_back(free_order ? free_order[i] : i);
+}
+
+int32_t BlockManager::seq_new() {
+  const int32_t id = next_id_++;
+  seqs_.emplace(id, Seq{});
+  return id;
+}
+
+int32_t BlockManager::take_block() {
+  const int32_t b = free_.front();
+  free_.pop_front();
+  ref_[b] = 1;
+  return b;
+}
+
+BmStatus BlockManager::append(int32_t seq, int32_t n, int64_t* slots, CowCopy* cow, int32_t* n_cow) {
+  auto it = seqs_.find(seq);
+  if (it == seqs_.end()) return BmStatus::kUnknownSeq;
+  if (n < 0) return BmStatus::kBadArg;
+  Seq& s = it->second;
+  const int32_t bs = block_size_;
+  *n_cow = 0;
+  if (n == 0) return BmStatus::kOk;
+  // Blocks this append takes from the queue: one copy target when the tail
+  // block is partially filled and shared, plus one per token that opens a block.
+  const bool copy_tail = (s.length % bs) != 0 && ref_[s.table.back()] > 1;
+  const int64_t first_new = (static_cast<int64_t>(s.length) + bs - 1) / bs;  // blocks in use
+  const int64_t last_new = (static_cast<int64_t>(s.length) + n + bs - 1) / bs;
+  const int64_t need = (last_new - first_new) + (copy_tail ? 1 : 0);
+  if (need > static_cast<int64_t>(free_.size())) return BmStatus::kNoBlocks;
+  if (copy_tail) {
+    const int32_t src = s.table.back();
+    const int32_t dst = take_block();
+    ref_[src] -= 1;
+    s.table.back() = dst;
+    cow->src = src;
+    cow->dst = dst;
+    cow->n_valid = s.length % bs;
+    *n_cow = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t pos = s.length + i;
+    if (pos % bs == 0) s.table.push_back(take_block());
+    slots[i] = static_cast<int64_t>(s.table[pos / bs]) * bs + pos % bs;
+  }
+  s.length += n;
+  return BmStatus::kOk;
+}
+
+BmStatus BlockManager::fork(int32_t parent, int32_t* child) {
+  auto it = seqs_.find(parent);
+  if (it == seqs_.end()) return BmStatus::kUnknownSeq;
+  Seq copy = it->second;
+  for (int32_t b : copy.table) ref_[b] += 1;
+  const int32_t id = next_id_++;
+  seqs_.emplace(id, std::move(copy));
+  *child = id;
+  return BmStatus::kOk;
+}
+
+BmStatus BlockManager::free_seq(int32_t seq) {
+  auto it = seqs_.find(seq);
+  if (it == seqs_.end()) return BmStatus::kUnknownSeq;
+  for (int32_t b : it->second.table) {
+    if (--ref_[b] == 0) free_.push_back(b);
+  }
+  seqs_.erase(it);
+  return BmStatus::kOk;
+}
+
+}  // namespace spork

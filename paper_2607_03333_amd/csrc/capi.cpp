@@ -1,0 +1,377 @@
+// C ABI of libspork (declared in include/spork.h): argument checks, error
+// reporting, block-manager and planner calls, kernel dispatch.
+#include "spork.h"
+
+#include <cmath>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <string>
+
+#include "block_manager.h"
+#include "kernels.h"
+#include "plan.h"
+
+struct spork_cache {
+  spork::BlockManager bm;
+  spork_cache(int32_t nb, int32_t bs, const int32_t* order) : bm(nb, bs, order) {}
+};
+
+struct spork_plan {
+  spork::Plan p;
+  spork_shape shape;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+constexpr int kAbiVersion = 1;
+
+int from_bm(spork::BmStatus s, const char* what) {
+  switch (s) {
+    case spork::BmStatus::kOk: return SPORK_OK;
+    case spork::BmStatus::kUnknownSeq: return fail(SPORK_E_INVAL, std::string(what) + ": unknown sequence id");
+    case spork::BmStatus::kBadArg: return fail(SPORK_E_INVAL, std::string(what) + ": bad argument");
+    case spork::BmStatus::kNoBlocks: return fail(SPORK_E_NOBLOCKS, std::string(what) + ": not enough free blocks");
+  }
+  return fail(SPORK_E_INVAL, what);
+}
+
+int elem_bytes(int32_t dtype) { return dtype == SPORK_DTYPE_BF16 ? 2 : (dtype == SPORK_DTYPE_F32 ? 4 : 0); }
+
+int check_shape(const spork_shape* sh) {
+  if (sh == nullptr) return fail(SPORK_E_INVAL, "shape is NULL");
+  if (sh->hq <= 0 || sh->hkv <= 0 || sh->hq % sh->hkv != 0)
+    return fail(SPORK_E_INVAL, "hq and hkv must be positive and hq a multiple of hkv");
+  if (sh->head_dim <= 0 || sh->block_size <= 0) return fail(SPORK_E_INVAL, "head_dim and block_size must be positive");
+  if (elem_bytes(sh->dtype) == 0) return fail(SPORK_E_UNSUPPORTED, "dtype must be SPORK_DTYPE_F32 or SPORK_DTYPE_BF16");
+  if (!std::isfinite(sh->sm_scale)) return fail(SPORK_E_INVAL, "sm_scale must be finite");
+  return SPORK_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <typename F>
+int guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(SPORK_E_INVAL, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(SPORK_E_INVAL, e.what());
+  } catch (...) {
+    return fail(SPORK_E_INVAL, "unknown error");
+  }
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return SPORK_OK;
+  return fail(SPORK_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* spork_last_error(void) { return g_last_error.c_str(); }
+
+int spork_version(void) { return kAbiVersion; }
+
+int spork_cache_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,
+                       spork_cache** out) {
+  return guarded([&] {
+    if (out == nullptr) return fail(SPORK_E_INVAL, "out is NULL");
+    if (num_blocks <= 0 || block_size <= 0) return fail(SPORK_E_INVAL, "num_blocks and block_size must be positive");
+    if (free_order != nullptr) {
+      std::string seen(static_cast<size_t>(num_blocks), '\0');
+      for (int32_t i = 0; i < num_blocks; ++i) {
+        const int32_t b = free_order[i];
+        if (b < 0 || b >= num_blocks || seen[b]) return fail(SPORK_E_INVAL, "free_order is not a permutation");
+        seen[b] = 1;
+      }
+    }
+    *out = new spork_cache(num_blocks, block_size, free_order);
+    return SPORK_OK;
+  });
+}
+
+int spork_cache_destroy(spork_cache* cache) {
+  delete cache;
+  return SPORK_OK;
+}
+
+int spork_seq_new(spork_cache* cache, int32_t* seq_out) {
+  return guarded([&] {
+    if (cache == nullptr || seq_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+    *seq_out = cache->bm.seq_new();
+    return SPORK_OK;
+  });
+}
+
+int spork_seq_append(spork_cache* cache, int32_t seq, int32_t n_tokens, int64_t* slots_out,
+                     int32_t* cow_out, int32_t* n_cow_out) {
+  return guarded([&] {
+    if (cache == nullptr || cow_out == nullptr || n_cow_out == nullptr || (n_tokens > 0 && slots_out == nullptr))
+      return fail(SPORK_E_INVAL, "NULL argument");
+    spork::CowCopy cow;
+    int32_t n_cow = 0;
+    const int rc = from_bm(cache->bm.append(seq, n_tokens, slots_out, &cow, &n_cow), "spork_seq_append");
+    if (rc != SPORK_OK) return rc;
+    *n_cow_out = n_cow;
+    cow_out[0] = cow.src;
+    cow_out[1] = cow.dst;
+    cow_out[2] = cow.n_valid;
+    return SPORK_OK;
+  });
+}
+
+int spork_fork(spork_cache* cache, int32_t parent_seq, int32_t* child_seq_out) {
+  return guarded([&] {
+    if (cache == nullptr || child_seq_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+    return from_bm(cache->bm.fork(parent_seq, child_seq_out), "spork_fork");
+  });
+}
+
+int spork_seq_free(spork_cache* cache, int32_t seq) {
+  return guarded([&] {
+    if (cache == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+    return from_bm(cache->bm.free_seq(seq), "spork_seq_free");
+  });
+}
+
+int spork_seq_len(const spork_cache* cache, int32_t seq, int32_t* len_out) {
+  if (cache == nullptr || len_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  if (!cache->bm.has(seq)) return fail(SPORK_E_INVAL, "spork_seq_len: unknown sequence id");
+  *len_out = cache->bm.length(seq);
+  return SPORK_OK;
+}
+
+int spork_block_table(const spork_cache* cache, int32_t seq, int32_t* out, int32_t cap, int32_t* n_out) {
+  if (cache == nullptr || n_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  if (!cache->bm.has(seq)) return fail(SPORK_E_INVAL, "spork_block_table: unknown sequence id");
+  const auto& t = cache->bm.table(seq);
+  *n_out = static_cast<int32_t>(t.size());
+  if (static_cast<int64_t>(t.size()) > cap) return fail(SPORK_E_CAPACITY, "spork_block_table: out too small");
+  if (!t.empty()) {
+    if (out == nullptr) return fail(SPORK_E_INVAL, "out is NULL");
+    std::memcpy(out, t.data(), t.size() * sizeof(int32_t));
+  }
+  return SPORK_OK;
+}
+
+int spork_refcount(const spork_cache* cache, int32_t block, int32_t* out) {
+  if (cache == nullptr || out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  if (block < 0 || block >= cache->bm.num_blocks()) return fail(SPORK_E_INVAL, "block out of range");
+  *out = cache->bm.refcount(block);
+  return SPORK_OK;
+}
+
+int spork_free_blocks(const spork_cache* cache, int32_t* out, int32_t cap, int32_t* n_out) {
+  if (cache == nullptr || n_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  const auto& q = cache->bm.free_queue();
+  *n_out = static_cast<int32_t>(q.size());
+  if (static_cast<int64_t>(q.size()) > cap) return fail(SPORK_E_CAPACITY, "spork_free_blocks: out too small");
+  if (!q.empty() && out == nullptr) return fail(SPORK_E_INVAL, "out is NULL");
+  int32_t i = 0;
+  for (int32_t b : q) out[i++] = b;
+  return SPORK_OK;
+}
+
+int spork_kv_write(const spork_shape* shape, void* k_cache, void* v_cache, int32_t num_blocks,
+                   const int64_t* slots, const void* k_new, const void* v_new, int32_t n,
+                   int32_t* bad_slots, hipStream_t stream) {
+  return guarded([&] {
+    int rc = check_shape(shape);
+    if (rc != SPORK_OK) return rc;
+    if (n < 0 || num_blocks <= 0) return fail(SPORK_E_INVAL, "n must be >= 0 and num_blocks > 0");
+    if (n == 0) return SPORK_OK;
+    if (!k_cache || !v_cache || !slots || !k_new || !v_new) return fail(SPORK_E_INVAL, "NULL pointer");
+    const int vec = 16 / elem_bytes(shape->dtype);
+    if (shape->head_dim % vec != 0) return fail(SPORK_E_UNSUPPORTED, "head_dim must fill 16-byte vectors");
+    if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) || !aligned16(v_new))
+      return fail(SPORK_E_INVAL, "pools and token arrays must be 16-byte aligned");
+    const int64_t num_slots = static_cast<int64_t>(num_blocks) * shape->block_size;
+    return hip_status(spork::launch_kv_write(shape->dtype, shape->hkv, shape->head_dim, shape->block_size,
+                                             num_slots, k_cache, v_cache, slots, k_new, v_new, n, bad_slots,
+                                             stream),
+                      "spork_kv_write");
+  });
+}
+
+int spork_kv_copy(const spork_shape* shape, void* k_cache, void* v_cache, int32_t num_blocks,
+                  int32_t src_block, int32_t dst_block, int32_t n_valid, hipStream_t stream) {
+  return guarded([&] {
+    int rc = check_shape(shape);
+    if (rc != SPORK_OK) return rc;
+    if (!k_cache || !v_cache) return fail(SPORK_E_INVAL, "NULL pointer");
+    if (src_block < 0 || src_block >= num_blocks || dst_block < 0 || dst_block >= num_blocks || src_block == dst_block)
+      return fail(SPORK_E_INVAL, "src/dst block out of range or equal");
+    if (n_valid < 0 || n_valid > shape->block_size) return fail(SPORK_E_INVAL, "n_valid out of range");
+    return hip_status(spork::launch_kv_copy(shape->dtype, shape->hkv, shape->head_dim, shape->block_size, k_cache,
+                                            v_cache, src_block, dst_block, n_valid, stream),
+                      "spork_kv_copy");
+  });
+}
+
+int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const int32_t* seqs,
+                      const int32_t* n_rows, const int32_t* groups, int32_t n_threads, int32_t n_cu,
+                      spork_plan** out) {
+  return guarded([&] {
+    if (cache == nullptr || out == nullptr || seqs == nullptr || n_rows == nullptr || groups == nullptr)
+      return fail(SPORK_E_INVAL, "NULL argument");
+    int rc = check_shape(shape);
+    if (rc != SPORK_OK) return rc;
+    spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype)};
+    auto* plan = new spork_plan();
+    plan->shape = *shape;
+    const std::string err = spork::build_plan(cache->bm, ps, seqs, n_rows, groups, n_threads, n_cu, &plan->p);
+    if (!err.empty()) {
+      delete plan;
+      return fail(SPORK_E_INVAL, "spork_plan_create: " + err);
+    }
+    *out = plan;
+    return SPORK_OK;
+  });
+}
+
+int spork_plan_destroy(spork_plan* plan) {
+  delete plan;
+  return SPORK_OK;
+}
+
+int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info) {
+  if (plan == nullptr || info == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  const spork::Plan& p = plan->p;
+  std::memset(info, 0, sizeof(*info));
+  info->n_threads = p.n_threads;
+  info->n_rows = p.n_rows;
+  info->n_groups = p.n_groups;
+  info->n_items = p.n_items;
+  info->n_waves = p.n_waves;
+  info->n_partials = p.n_partials;
+  info->max_row_tiles = p.row_tiles;
+  info->image_bytes = p.image.size();
+  info->workspace_bytes = p.workspace_bytes;
+  info->shared_tokens = p.shared_tokens;
+  info->private_tokens = p.private_tokens;
+  const int64_t per_tok = 2LL * p.shape.hkv * p.shape.head_dim * p.shape.elem_bytes;
+  info->unique_kv_bytes = (p.shared_tokens + p.private_tokens) * per_tok;
+  info->flat_kv_bytes = p.flat_tokens * per_tok;
+  return SPORK_OK;
+}
+
+int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap) {
+  if (plan == nullptr || host_dst == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+  if (cap < plan->p.image.size()) return fail(SPORK_E_CAPACITY, "spork_plan_image: destination too small");
+  std::memcpy(host_dst, plan->p.image.data(), plan->p.image.size());
+  return SPORK_OK;
+}
+
+static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                     const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
+                     hipStream_t stream) {
+  const spork::Plan& p = plan->p;
+  const spork_shape& sh = plan->shape;
+  if (!spork::attention_supported(sh.dtype, sh.head_dim, sh.block_size, p.row_tiles))
+    return fail(SPORK_E_UNSUPPORTED, "no attention kernel for this dtype / head_dim / block_size / row tiles "
+                                     "(bf16: head_dim 128; f32: head_dim 64 or 128; block_size 16 or 32)");
+  if (!dev_image || !q || !k_cache || !v_cache || !out) return fail(SPORK_E_INVAL, "NULL pointer");
+  if ((reinterpret_cast<uintptr_t>(dev_image) & 255) != 0) return fail(SPORK_E_INVAL, "dev_image must be 256-byte aligned");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(SPORK_E_INVAL, "q, pools and out must be 16-byte aligned");
+  if (ws_bytes < p.workspace_bytes) return fail(SPORK_E_CAPACITY, "workspace smaller than info.workspace_bytes");
+  if (p.workspace_bytes > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
+    return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
+  const auto* img = static_cast<const uint8_t*>(dev_image);
+  spork::AttnArgs a{};
+  a.waves = reinterpret_cast<const spork::WaveDesc*>(img + p.off_waves);
+  a.items = reinterpret_cast<const spork::ItemDesc*>(img + p.off_items);
+  a.rows = reinterpret_cast<const spork::RowDesc*>(img + p.off_rows);
+  a.tables = reinterpret_cast<const int32_t*>(img + p.off_tables);
+  a.merge_off = reinterpret_cast<const int32_t*>(img + p.off_merge_off);
+  a.merge_ids = reinterpret_cast<const int32_t*>(img + p.off_merge_ids);
+  a.n_waves = p.n_waves;
+  a.n_out = p.n_out;
+  a.row_tiles = p.row_tiles;
+  a.hq = sh.hq;
+  a.hkv = sh.hkv;
+  a.head_dim = sh.head_dim;
+  a.block_size = sh.block_size;
+  a.dtype = sh.dtype;
+  a.scale_log2 = sh.sm_scale * 1.4426950408889634f;
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.out = out;
+  a.lse = lse;
+  a.part_o = static_cast<float*>(workspace);
+  a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
+  return hip_status(spork::launch_attention(a, stream), "spork_attn_decode");
+}
+
+int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                      const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
+                      hipStream_t stream) {
+  return guarded([&] {
+    if (plan == nullptr) return fail(SPORK_E_INVAL, "plan is NULL");
+    return attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, stream);
+  });
+}
+
+int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return fail(SPORK_E_INVAL, "bytes is NULL");
+  if (n_verify < 0 || k_drafts < 0 || vocab <= 0) return fail(SPORK_E_INVAL, "bad sizes");
+  const int32_t rows = n_verify * (k_drafts + 1);
+  *bytes = static_cast<size_t>(rows) * spork::accept_chunks(rows, vocab) * sizeof(uint64_t);
+  return SPORK_OK;
+}
+
+int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                        const void* v_cache, void* out, float* lse, const void* logits, int32_t logits_dtype,
+                        int32_t vocab, const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
+                        int32_t* accept_len, int32_t* next_token, int32_t* argmax_out, void* workspace,
+                        size_t ws_bytes, hipStream_t stream) {
+  return guarded([&] {
+    if (n_verify < 0 || k_drafts < 0 || k_drafts > 4096 || vocab <= 0)
+      return fail(SPORK_E_INVAL, "n_verify >= 0, 0 <= k_drafts <= 4096 and vocab > 0 required");
+    if (logits_dtype != SPORK_DTYPE_F32 && logits_dtype != SPORK_DTYPE_BF16)
+      return fail(SPORK_E_UNSUPPORTED, "logits dtype must be f32 or bf16");
+    const int64_t rows = static_cast<int64_t>(n_verify) * (k_drafts + 1);
+    if (rows * static_cast<int64_t>(vocab) > (static_cast<int64_t>(1) << 40)) return fail(SPORK_E_INVAL, "logits too large");
+    if (n_verify > 0 && (!logits || !accept_len || !next_token || (k_drafts > 0 && !drafts)))
+      return fail(SPORK_E_INVAL, "NULL pointer");
+    size_t att_ws = 0;
+    if (plan != nullptr) att_ws = (plan->p.workspace_bytes + 255) & ~static_cast<size_t>(255);
+    size_t acc_ws = 0;
+    spork_verify_workspace_bytes(n_verify, k_drafts, vocab, &acc_ws);
+    if (ws_bytes < att_ws + acc_ws) return fail(SPORK_E_CAPACITY, "workspace too small for attention + accept");
+    if ((att_ws + acc_ws) > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
+      return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
+    if (plan != nullptr) {
+      const int rc = attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, stream);
+      if (rc != SPORK_OK) return rc;
+    }
+    if (n_verify == 0) return SPORK_OK;
+    spork::AcceptArgs a{};
+    a.logits = logits;
+    a.logits_dtype = logits_dtype;
+    a.vocab = vocab;
+    a.n_verify = n_verify;
+    a.k_drafts = k_drafts;
+    a.chunks = spork::accept_chunks(static_cast<int32_t>(rows), vocab);
+    a.drafts = drafts;
+    a.accept_len = accept_len;
+    a.next_token = next_token;
+    a.argmax_out = argmax_out;
+    a.keys = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(workspace) + att_ws);
+    return hip_status(spork::launch_accept(a, stream), "spork_verify_accept");
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,56 @@
+// Launch interface between the C ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "plan_types.h"
+
+namespace spork {
+
+struct AttnArgs {
+  const WaveDesc* waves;
+  const ItemDesc* items;
+  const RowDesc* rows;
+  const int32_t* tables;
+  const int32_t* merge_off;
+  const int32_t* merge_ids;
+  int32_t n_waves, n_out, row_tiles;
+  int32_t hq, hkv, head_dim, block_size, dtype;
+  float scale_log2;  // sm_scale * log2(e): scores are kept in base 2
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  void* out;
+  float* lse;
+  float* part_o;   // [n_partials][head_dim] unnormalised partial outputs
+  float* part_ml;  // [n_partials][2] running max (base 2) and sum
+};
+
+// true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
+bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles);
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+
+struct AcceptArgs {
+  const void* logits;
+  int32_t logits_dtype, vocab, n_verify, k_drafts, chunks;
+  const int32_t* drafts;
+  int32_t* accept_len;
+  int32_t* next_token;
+  int32_t* argmax_out;
+  uint64_t* keys;  // [rows][chunks] workspace
+};
+int32_t accept_chunks(int32_t rows, int32_t vocab);
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream);
+
+hipError_t launch_kv_write(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
+                           int64_t num_slots, void* k_cache, void* v_cache, const int64_t* slots,
+                           const void* k_new, const void* v_new, int32_t n, int32_t* bad_slots,
+                           hipStream_t stream);
+hipError_t launch_kv_copy(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
+                          void* k_cache, void* v_cache, int32_t src, int32_t dst, int32_t n_valid,
+                          hipStream_t stream);
+
+}  // namespace spork

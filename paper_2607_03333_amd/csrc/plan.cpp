@@ -1,0 +1,277 @@
+#include "plan.h"
+
+#include <algorithm>
+#include <climits>
+#include <cstring>
+#include <map>
+
+namespace spork {
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// A context range [lo, hi) read by the rows of `threads`, through the block
+// table of `table_thread` (all of them share those blocks).
+struct Range {
+  int32_t lo, hi;
+  int32_t table_thread;
+  std::vector<int32_t> threads;
+};
+
+struct Unit {  // one token segment of one item, split over `slices` row slices
+  int32_t item, lo, hi, slices;
+  int64_t cost() const { return static_cast<int64_t>(hi - lo) * slices; }
+};
+
+}  // namespace
+
+std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int32_t* seqs,
+                       const int32_t* n_rows, const int32_t* groups, int32_t n_threads,
+                       int32_t n_cu, Plan* out) {
+  if (shape.hq <= 0 || shape.hkv <= 0 || shape.hq % shape.hkv != 0)
+    return "hq and hkv must be positive with hq a multiple of hkv";
+  if (shape.head_dim <= 0 || shape.block_size <= 0) return "head_dim and block_size must be positive";
+  if (shape.block_size != bm.block_size()) return "shape.block_size differs from the cache's block size";
+  if (n_threads <= 0) return "n_threads must be positive";
+  if (n_cu <= 0) n_cu = 256;
+  const int32_t bs = shape.block_size, hq = shape.hq, hkv = shape.hkv, gq = hq / hkv;
+
+  std::vector<int32_t> len(n_threads), row_base(n_threads + 1, 0);
+  for (int32_t t = 0; t < n_threads; ++t) {
+    if (!bm.has(seqs[t])) return "unknown sequence id " + std::to_string(seqs[t]);
+    len[t] = bm.length(seqs[t]);
+    if (n_rows[t] < 1 || n_rows[t] > len[t])
+      return "thread " + std::to_string(t) + ": n_rows must be in [1, sequence length]";
+    row_base[t + 1] = row_base[t] + n_rows[t];
+  }
+  const int64_t total_rows = row_base[n_threads];
+  if (total_rows * hq > INT32_MAX / 2) return "batch too large";
+
+  // Fork groups in order of first appearance; -1 stands alone.
+  std::vector<std::vector<int32_t>> members;
+  std::map<int32_t, size_t> gid;
+  for (int32_t t = 0; t < n_threads; ++t) {
+    if (groups[t] < 0) {
+      members.push_back({t});
+      continue;
+    }
+    auto it = gid.find(groups[t]);
+    if (it == gid.end()) {
+      gid.emplace(groups[t], members.size());
+      members.push_back({t});
+    } else {
+      members[it->second].push_back(t);
+    }
+  }
+
+  Plan p;
+  p.shape = shape;
+  p.n_threads = n_threads;
+  p.n_rows = static_cast<int32_t>(total_rows);
+  p.n_groups = static_cast<int32_t>(members.size());
+
+  std::vector<Range> ranges;
+  for (const auto& m : members) {
+    for (int32_t t : m) p.flat_tokens += len[t];
+    if (m.size() == 1) {
+      const int32_t t = m[0];
+      ranges.push_back({0, len[t], t, {t}});
+      p.private_tokens += len[t];
+      continue;
+    }
+    // Longest common prefix of the members' tables, in whole blocks ...
+    size_t lcp = bm.table(seqs[m[0]]).size();
+    for (int32_t t : m) lcp = std::min(lcp, bm.table(seqs[t]).size());
+    const auto& t0 = bm.table(seqs[m[0]]);
+    size_t i = 0;
+    for (; i < lcp; ++i) {
+      bool same = true;
+      for (int32_t t : m) same = same && bm.table(seqs[t])[i] == t0[i];
+      if (!same) break;
+    }
+    // ... capped so that every row of every member sees the whole prefix.
+    int64_t shared = static_cast<int64_t>(i) * bs;
+    for (int32_t t : m) shared = std::min<int64_t>(shared, len[t] - n_rows[t] + 1);
+    const int32_t P = static_cast<int32_t>(shared);
+    if (P > 0) {
+      ranges.push_back({0, P, m[0], m});
+      p.shared_tokens += P;
+    }
+    for (int32_t t : m) {
+      if (len[t] > P) {
+        ranges.push_back({P, len[t], t, {t}});
+        p.private_tokens += len[t] - P;
+      }
+    }
+  }
+
+  // Row tiles per workgroup: large row sets are split into near-equal slices
+  // of at most kMaxRowTiles tiles; every workgroup of the launch uses the
+  // largest slice size.
+  int32_t row_tiles = 1;
+  std::vector<int32_t> range_rows(ranges.size());
+  for (size_t r = 0; r < ranges.size(); ++r) {
+    int32_t rows = 0;
+    for (int32_t t : ranges[r].threads) rows += n_rows[t] * gq;
+    range_rows[r] = rows;
+    const int32_t tiles = (rows + 15) / 16;
+    const int32_t slices = (tiles + kMaxRowTiles - 1) / kMaxRowTiles;
+    row_tiles = std::max(row_tiles, (tiles + slices - 1) / slices);
+  }
+  const int32_t slice_rows = row_tiles * 16;
+  p.row_tiles = row_tiles;
+
+  // Items (range x KV head), their rows and the block tables.
+  std::vector<int32_t> table_off(n_threads, -1);
+  std::vector<int32_t> tables;
+  std::vector<ItemDesc> items;
+  std::vector<RowDesc> rows;
+  std::vector<Range*> item_range;
+  for (size_t r = 0; r < ranges.size(); ++r) {
+    Range& rg = ranges[r];
+    const int32_t tt = rg.table_thread;
+    if (table_off[tt] < 0) {
+      table_off[tt] = static_cast<int32_t>(tables.size());
+      const auto& tb = bm.table(seqs[tt]);
+      tables.insert(tables.end(), tb.begin(), tb.end());
+    }
+    for (int32_t h = 0; h < hkv; ++h) {
+      ItemDesc it{};
+      it.kv_head = h;
+      it.table_off = table_off[tt];
+      it.n_blocks = static_cast<int32_t>(bm.table(seqs[tt]).size());
+      it.row_off = static_cast<int32_t>(rows.size());
+      it.n_rows = range_rows[r];
+      for (int32_t t : rg.threads)
+        for (int32_t q = 0; q < n_rows[t]; ++q)
+          for (int32_t j = 0; j < gq; ++j)
+            rows.push_back({(row_base[t] + q) * hq + h * gq + j, len[t] - n_rows[t] + q});
+      items.push_back(it);
+      item_range.push_back(&rg);
+    }
+  }
+  p.n_items = static_cast<int32_t>(items.size());
+
+  // Split-K: cut every item into token segments of near-equal cost so that
+  // about one full-occupancy wave of workgroups covers the batch.
+  const int32_t waves_per_cu = row_tiles <= 2 ? 8 : 4;
+  const int64_t target = static_cast<int64_t>(n_cu) * waves_per_cu;
+  int64_t cost = 0;
+  for (size_t it = 0; it < items.size(); ++it) {
+    const Range& rg = *item_range[it];
+    const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
+    cost += static_cast<int64_t>(rg.hi - rg.lo) * slices;
+  }
+  int64_t seg = (cost + target - 1) / target;
+  seg = std::max<int64_t>(kTileTokens, (seg + kTileTokens - 1) / kTileTokens * kTileTokens);
+
+  std::vector<Unit> units;
+  for (size_t it = 0; it < items.size(); ++it) {
+    const Range& rg = *item_range[it];
+    const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
+    const int64_t n = rg.hi - rg.lo;
+    const int64_t nseg = std::max<int64_t>(1, (n + seg - 1) / seg);
+    int32_t lo = rg.lo;
+    for (int64_t k = 1; k <= nseg; ++k) {
+      int32_t hi = rg.hi;
+      if (k < nseg) {
+        const int64_t cut = rg.lo + n * k / nseg;
+        hi = static_cast<int32_t>(cut / kTileTokens * kTileTokens);
+        if (hi <= lo) continue;
+      }
+      units.push_back({static_cast<int32_t>(it), lo, hi, slices});
+      lo = hi;
+    }
+  }
+
+  // Longest first, each unit to the least-loaded die; a unit's row slices are
+  // adjacent in its die's queue so they run together and share that die's L2.
+  std::stable_sort(units.begin(), units.end(),
+                   [](const Unit& a, const Unit& b) { return a.hi - a.lo > b.hi - b.lo; });
+  std::vector<std::vector<WaveDesc>> queue(kXcds);
+  std::vector<int64_t> load(kXcds, 0);
+  for (const Unit& u : units) {
+    const int x = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += u.cost();
+    const int32_t nr = items[u.item].n_rows;
+    for (int32_t s = 0; s < u.slices; ++s) {
+      WaveDesc w{};
+      w.item = u.item;
+      w.tok_lo = u.lo;
+      w.tok_hi = u.hi;
+      w.row0 = s * slice_rows;
+      w.nrows = std::min(slice_rows, nr - s * slice_rows);
+      queue[x].push_back(w);
+    }
+  }
+  size_t depth = 0;
+  for (const auto& q : queue) depth = std::max(depth, q.size());
+  std::vector<WaveDesc> waves;
+  waves.reserve(depth * kXcds);
+  int32_t partial = 0;
+  for (size_t d = 0; d < depth; ++d) {
+    for (int x = 0; x < kXcds; ++x) {
+      if (d < queue[x].size()) {
+        WaveDesc w = queue[x][d];
+        w.partial = partial;
+        partial += w.nrows;
+        waves.push_back(w);
+      } else {
+        waves.push_back({-1, 0, 0, 0, 0, 0});
+      }
+    }
+  }
+  p.n_waves = static_cast<int32_t>(waves.size());
+  p.n_partials = partial;
+
+  // Merge lists: the partial rows of every output (query row x query head).
+  p.n_out = static_cast<int32_t>(total_rows * hq);
+  std::vector<int32_t> count(p.n_out + 1, 0);
+  for (const WaveDesc& w : waves) {
+    if (w.item < 0) continue;
+    for (int32_t i = 0; i < w.nrows; ++i) count[rows[items[w.item].row_off + w.row0 + i].qidx + 1]++;
+  }
+  for (int32_t o = 0; o < p.n_out; ++o) {
+    if (count[o + 1] == 0) return "internal: output without a partial";
+    count[o + 1] += count[o];
+  }
+  std::vector<int32_t> merge_ids(count[p.n_out]);
+  std::vector<int32_t> fill(count.begin(), count.end() - 1);
+  for (const WaveDesc& w : waves) {
+    if (w.item < 0) continue;
+    for (int32_t i = 0; i < w.nrows; ++i)
+      merge_ids[fill[rows[items[w.item].row_off + w.row0 + i].qidx]++] = w.partial + i;
+  }
+
+  // Device image.
+  size_t off = 0;
+  auto place = [&](size_t bytes) {
+    const size_t at = off;
+    off = align256(off + bytes);
+    return at;
+  };
+  p.off_waves = place(waves.size() * sizeof(WaveDesc));
+  p.off_items = place(items.size() * sizeof(ItemDesc));
+  p.off_rows = place(rows.size() * sizeof(RowDesc));
+  p.off_tables = place(tables.size() * sizeof(int32_t));
+  p.off_merge_off = place(count.size() * sizeof(int32_t));
+  p.off_merge_ids = place(merge_ids.size() * sizeof(int32_t));
+  p.image.assign(off, 0);
+  auto put = [&](size_t at, const void* src, size_t bytes) {
+    if (bytes) std::memcpy(p.image.data() + at, src, bytes);
+  };
+  put(p.off_waves, waves.data(), waves.size() * sizeof(WaveDesc));
+  put(p.off_items, items.data(), items.size() * sizeof(ItemDesc));
+  put(p.off_rows, rows.data(), rows.size() * sizeof(RowDesc));
+  put(p.off_tables, tables.data(), tables.size() * sizeof(int32_t));
+  put(p.off_merge_off, count.data(), count.size() * sizeof(int32_t));
+  put(p.off_merge_ids, merge_ids.data(), merge_ids.size() * sizeof(int32_t));
+
+  const size_t o_bytes = align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
+  p.off_ws_ml = o_bytes;
+  p.workspace_bytes = o_bytes + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
+  *out = std::move(p);
+  return "";
+}
+
+}  // namespace spork

@@ -1,0 +1,44 @@
+// Host planner: turns a batch of forked threads into the attention work list.
+//
+// Threads of one fork group share the longest common prefix of their block
+// tables (capped so that every row may see all of it); that prefix is one
+// work item per KV head whose rows are all members' rows, so its KV is read
+// once per group. Each thread's remaining positions form its own item. Items
+// are cut into token ranges of near-equal size (split-K), one workgroup per
+// (range, row slice), and every output row lists the partial results the
+// log-sum-exp merge combines.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "block_manager.h"
+#include "plan_types.h"
+
+namespace spork {
+
+struct PlanShape {
+  int32_t hq, hkv, head_dim, block_size, elem_bytes;
+};
+
+struct Plan {
+  PlanShape shape{};
+  int32_t n_threads = 0, n_rows = 0, n_groups = 0, n_items = 0;
+  int32_t n_waves = 0, n_partials = 0, row_tiles = 1, n_out = 0;
+  int64_t shared_tokens = 0, private_tokens = 0, flat_tokens = 0;
+  // device image: sections at 256-byte aligned byte offsets
+  std::vector<uint8_t> image;
+  size_t off_waves = 0, off_items = 0, off_rows = 0, off_tables = 0, off_merge_off = 0,
+         off_merge_ids = 0;
+  size_t workspace_bytes = 0;  // partial outputs + (m, l) pairs
+  size_t off_ws_ml = 0;        // byte offset of the (m, l) pairs in the workspace
+};
+
+// Returns "" on success, else an error message (nothing is built).
+std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int32_t* seqs,
+                       const int32_t* n_rows, const int32_t* groups, int32_t n_threads,
+                       int32_t n_cu, Plan* out);
+
+}  // namespace spork

@@ -1,0 +1,39 @@
+// Work descriptors shared by the host planner and the device kernels.
+#pragma once
+#include <cstdint>
+
+namespace spork {
+
+// One attention workgroup: a token range of one work item and a slice of the
+// item's query rows. item < 0 marks a padding workgroup that exits at once.
+struct WaveDesc {
+  int32_t item;
+  int32_t tok_lo;   // first context position of the range
+  int32_t tok_hi;   // one past the last position
+  int32_t row0;     // first row of the slice inside the item's row list
+  int32_t nrows;    // rows in the slice (<= 16 * row tiles of the kernel)
+  int32_t partial;  // first partial-result row this workgroup writes
+};
+
+// A (prefix or private) context range of one KV head and the rows reading it.
+struct ItemDesc {
+  int32_t kv_head;
+  int32_t table_off;  // offset of the block table in the image's table area
+  int32_t n_blocks;   // valid entries of that table
+  int32_t row_off;    // offset of the item's rows in the row area
+  int32_t n_rows;
+  int32_t pad;
+};
+
+// One query row of an item: output index (query row * Hq + query head) and
+// the last context position it may attend to.
+struct RowDesc {
+  int32_t qidx;
+  int32_t horizon;
+};
+
+constexpr int kTileTokens = 32;   // tokens per inner-loop tile
+constexpr int kMaxRowTiles = 4;   // 16-row MFMA tiles per workgroup (register budget)
+constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, workgroups dealt round-robin
+
+}  // namespace spork

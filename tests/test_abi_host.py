@@ -1,0 +1,230 @@
+"""Host side of the C ABI, on the CPU: exports, block manager parity with the
+oracle (bit-exact tables, slots, copies, refcounts and free queue), error
+codes, and planner invariants."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+from paper_2607_03333_amd import spork, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "spork.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spork_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(spork.LIB_PATH)
+    names = _declared_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(spork._SIGNATURES)
+    assert spork.spork_version() == 1
+
+
+def _apply_both(ops, nb, bs, order):
+    bm = oracle.BlockManager(nb, bs, order)
+    c = spork.spork_cache_create(nb, bs, order)
+    try:
+        live = []
+        for op in ops:
+            kind = op[0]
+            if kind == "new":
+                assert spork.spork_seq_new(c) == bm.seq_new()
+                live.append(max(bm.tables))
+            elif not live:
+                continue
+            elif kind == "append":
+                s = live[op[1] % len(live)]
+                try:
+                    slots, cow = bm.append(s, op[2])
+                except oracle.NoBlocksError:
+                    with pytest.raises(spork.SporkError) as ei:
+                        spork.spork_seq_append(c, s, op[2])
+                    assert ei.value.code == spork.SPORK_E_NOBLOCKS
+                    continue
+                gs, gc = spork.spork_seq_append(c, s, op[2])
+                assert gs.tolist() == slots and gc == cow
+            elif kind == "fork":
+                p = live[op[1] % len(live)]
+                assert spork.spork_fork(c, p) == bm.fork(p)
+                live.append(max(bm.tables))
+            elif kind == "free":
+                s = live.pop(op[1] % len(live))
+                bm.free_seq(s)
+                spork.spork_seq_free(c, s)
+            for s in live:
+                assert spork.spork_block_table(c, s).tolist() == bm.table(s)
+                assert spork.spork_seq_len(c, s) == bm.length(s)
+            assert [spork.spork_refcount(c, b) for b in range(nb)] == bm.ref
+            assert spork.spork_free_blocks(c).tolist() == bm.free_list()
+    finally:
+        spork.spork_cache_destroy(c)
+
+
+_op = st.one_of(
+    st.tuples(st.just("new")),
+    st.tuples(st.just("append"), st.integers(0, 7), st.integers(0, 9)),
+    st.tuples(st.just("fork"), st.integers(0, 7)),
+    st.tuples(st.just("free"), st.integers(0, 7)),
+)
+
+
+@settings(max_examples=300, deadline=None)
+@given(ops=st.lists(_op, min_size=1, max_size=30), nb=st.integers(1, 12), bs=st.sampled_from([1, 2, 4, 16]),
+       seed=st.integers(0, 1000))
+def test_block_manager_matches_oracle(ops, nb, bs, seed):
+    order = list(np.random.default_rng(seed).permutation(nb))
+    _apply_both([("new",)] + ops, nb, bs, order)
+
+
+def test_golden_trace_through_abi():
+    import json
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "block_manager_trace.json")))
+    c = spork.spork_cache_create(g["num_blocks"], g["block_size"], g["free_order"])
+    for op in g["ops"]:
+        if op["op"] == "new":
+            assert spork.spork_seq_new(c) == op["expect_seq"]
+        elif op["op"] == "fork":
+            assert spork.spork_fork(c, op["parent"]) == op["expect_seq"]
+        elif op["op"] == "append":
+            if op.get("expect_error"):
+                with pytest.raises(spork.SporkError):
+                    spork.spork_seq_append(c, op["seq"], op["n"])
+            else:
+                slots, cow = spork.spork_seq_append(c, op["seq"], op["n"])
+                assert slots.tolist() == op["expect_slots"] and [list(x) for x in cow] == op["expect_cow"]
+        elif op["op"] == "free":
+            spork.spork_seq_free(c, op["seq"])
+    assert spork.spork_free_blocks(c).tolist() == g["final"]["free_queue"]
+    assert spork.spork_block_table(c, 2).tolist() == g["final"]["tables"]["2"]
+    spork.spork_cache_destroy(c)
+
+
+def test_error_codes():
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_cache_create(4, 16, [0, 1, 1, 2])
+    assert e.value.code == spork.SPORK_E_INVAL
+    c = spork.spork_cache_create(4, 16)
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_fork(c, 3)
+    assert e.value.code == spork.SPORK_E_INVAL
+    s = spork.spork_seq_new(c)
+    spork.spork_seq_append(c, s, 20)
+    shape = spork.make_shape(4, 2, 64, 16, spork.SPORK_DTYPE_F32, 0.125)
+    with pytest.raises(spork.SporkError):
+        spork.spork_plan_create(c, shape, [s], [21], [0])          # more rows than tokens
+    with pytest.raises(spork.SporkError):
+        spork.spork_plan_create(c, spork.make_shape(4, 3, 64, 16, 0, 1.0), [s], [1], [0])
+    with pytest.raises(spork.SporkError):
+        spork.spork_plan_create(c, spork.make_shape(4, 2, 64, 8, 0, 1.0), [s], [1], [0])  # block size mismatch
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_plan_create(c, spork.make_shape(4, 2, 64, 16, 7, 1.0), [s], [1], [0])
+    assert e.value.code == spork.SPORK_E_UNSUPPORTED
+    p = spork.spork_plan_create(c, shape, [s], [1], [0])
+    # attention with a NULL image is rejected before any launch (no GPU needed)
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_attn_decode(p, 0, 0, 0, 0, 0, None, None, stream=0)
+    assert e.value.code in (spork.SPORK_E_INVAL, spork.SPORK_E_CAPACITY)
+    # unsupported head dim for bf16
+    p2 = spork.spork_plan_create(c, spork.make_shape(4, 2, 64, 16, spork.SPORK_DTYPE_BF16, 1.0), [s], [1], [0])
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_attn_decode(p2, 256, 256, 256, 256, 256, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_UNSUPPORTED
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_verify_accept(None, 0, 0, 0, 0, 0, None, 0, 5, 100, 0, 1, 2, 0, 0, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_UNSUPPORTED
+    for h in (p, p2):
+        spork.spork_plan_destroy(h)
+    spork.spork_cache_destroy(c)
+
+
+def _plan_for(wl, groups=None, n_cu=256):
+    c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
+    for stp in wl.steps:
+        for op in stp.ops_before:
+            if op[0] == "new":
+                spork.spork_seq_new(c)
+            elif op[0] == "append":
+                spork.spork_seq_append(c, op[1], op[2])
+            else:
+                spork.spork_fork(c, op[1])
+    stp = wl.steps[-1]
+    shape = spork.make_shape(wl.hq, wl.hkv, wl.d, wl.block_size,
+                             spork.SPORK_DTYPE_BF16 if wl.dtype == synth.BF16 else spork.SPORK_DTYPE_F32,
+                             wl.sm_scale)
+    p = spork.spork_plan_create(c, shape, stp.seqs, stp.n_rows, stp.groups if groups is None else groups, n_cu)
+    return c, p
+
+
+def _decode_image(p):
+    info = spork.spork_plan_get_info(p)
+    img = spork.spork_plan_image(p)
+    return info, img
+
+
+@pytest.mark.parametrize("index", [0, 1, 2, 3, 4])
+def test_plan_unique_bytes_match_workload(index):
+    shrink = {} if index == 0 else dict(sessions=3, prefix=256, suffix=("uniform", 1, 300))
+    if index == 3:
+        shrink = dict(sessions=3, prefix=256, vocab=1000)
+    wl = synth.make(index, **shrink)
+    c, p = _plan_for(wl)
+    info = spork.spork_plan_get_info(p)
+    assert info["unique_kv_bytes"] == wl.unique_kv_bytes(len(wl.steps) - 1)
+    assert info["n_rows"] == sum(wl.steps[-1].n_rows)
+    assert info["unique_kv_bytes"] <= info["flat_kv_bytes"]
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+def test_plan_covers_every_output_once_per_token():
+    """Decode the image: for every output (query row, head), the workgroups
+    that write one of its partials cover each visible position exactly once."""
+    wl = synth.make(4, sessions=3, prefix=200, suffix=("uniform", 1, 90))
+    c, p = _plan_for(wl, n_cu=4)
+    info, img = _decode_image(p)
+    raw = img.view(np.int32)
+    # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, merge_ids
+    nw = info["n_waves"]
+    waves = raw[: nw * 6].reshape(nw, 6)
+    off = -(-nw * 24 // 256) * 256 // 4
+    items = raw[off: off + info["n_items"] * 6].reshape(-1, 6)
+    off += -(-info["n_items"] * 24 // 256) * 256 // 4
+    nrow_desc = int(items[:, 4].sum())
+    rows = raw[off: off + 2 * nrow_desc].reshape(-1, 2)
+    stp = wl.steps[-1]
+    cover = {}
+    for w in waves:
+        item, lo, hi, row0, nr, part = (int(x) for x in w)
+        if item < 0:
+            continue
+        it = items[item]
+        for i in range(nr):
+            qidx, hz = rows[it[3] + row0 + i]
+            cover.setdefault(int(qidx), []).append((lo, min(hi, hz + 1)))
+    assert len(cover) == sum(stp.n_rows) * wl.hq
+    row = 0
+    lens = {s: 0 for s in stp.seqs}
+    for s in stp.seqs:
+        lens[s] = spork.spork_seq_len(c, s)
+    for s, n in zip(stp.seqs, stp.n_rows):
+        for r in range(n):
+            for h in range(wl.hq):
+                pos = lens[s] - n + r
+                seen = np.zeros(lens[s], dtype=int)
+                for lo, hi in cover[(row + r) * wl.hq + h]:
+                    seen[lo:hi] += 1
+                assert seen[: pos + 1].min() == 1 and seen[: pos + 1].max() == 1
+        row += n
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)

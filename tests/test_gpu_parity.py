@@ -1,0 +1,112 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, element by
+element, on the five workloads (shrunk so the oracle finishes in seconds while
+spanning several tiles, ragged tails and copy-on-write forks), plus the
+invariants the method guarantees."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_03333_amd import runner, spork, synth
+from gpu_cases import compare_attention, run_workload, say
+
+pytestmark = pytest.mark.gpu
+
+
+def test_tiny_fork_full_size():
+    """Tiny fork as specified: fp32, decode of main + probe, then the K=4 verify."""
+    wl = synth.make(0)
+    dw = run_workload(wl, "tiny-fork")
+    assert dw.steps[1].accept_len.cpu().tolist() == [2]
+    dw.close()
+
+
+@pytest.mark.parametrize("index,shrink", [
+    (1, dict(sessions=3, prefix=512, suffix=("uniform", 1, 300))),
+    (2, dict(sessions=2, prefix=1024, suffix=("uniform", 1, 200))),
+    (3, dict(sessions=3, prefix=700, vocab=5000)),
+    (4, dict(sessions=3, prefix=1000, suffix=("loguniform", 1, 400), vocab=3000)),
+])
+def test_workloads_shrunk(index, shrink):
+    wl = synth.make(index, **shrink)
+    run_workload(wl, f"{wl.name}-shrunk").close()
+
+
+def test_unaligned_fork_point_exercises_copy_on_write():
+    """Prefix of 1000 tokens (not a multiple of 16): every fork's first append
+    copies the shared partial block; the cascade then shares 62 whole blocks."""
+    wl = synth.make(2, sessions=2, prefix=1000, suffix=("uniform", 20, 80))
+    run_workload(wl, "cow").close()
+
+
+def test_sharp_softmax():
+    wl = synth.make(2, sessions=2, prefix=512, suffix=("uniform", 1, 100), q_gain=8.0)
+    run_workload(wl, "sharp").close()
+
+
+def test_single_token_contexts_and_all_rows():
+    """Threads of length 1, and verify rows covering a whole short context."""
+    wl = synth.make(3, sessions=2, prefix=1, vocab=600, verify_k=3)
+    # prefix 1 + 3 drafts -> L = 4 with 4 rows: every row sees a different count
+    run_workload(wl, "short").close()
+
+
+def test_fork_without_suffix_equals_parent_bit_exact():
+    wl = synth.make(2, sessions=1, prefix=777, suffix=("fixed", [0]))
+    wl.steps[0].q[:] = wl.steps[0].q[0]           # same query for main and probes
+    dw = run_workload(wl, "nosuffix")
+    out = dw.steps[0].out.view(torch.int16)
+    for t in range(1, out.shape[0]):
+        assert torch.equal(out[0], out[t])
+    dw.close()
+
+
+def test_block_placement_does_not_change_results():
+    wl = synth.make(4, sessions=2, prefix=300, suffix=("uniform", 1, 120), vocab=1000)
+    dw1 = run_workload(wl, "placement-a", repeat_check=False)
+    o1 = dw1.steps[0].out.view(torch.int16).clone()
+    dw1.close()
+    wl.free_order = np.random.default_rng(5).permutation(wl.num_blocks).astype(np.int32)
+    dw2 = run_workload(wl, "placement-b", repeat_check=False)
+    assert torch.equal(o1, dw2.steps[0].out.view(torch.int16))
+    dw2.close()
+
+
+def test_cascade_matches_flat():
+    """Groups = -1 (every thread reads its whole context) against the cascade."""
+    wl = synth.make(2, sessions=2, prefix=900, suffix=("uniform", 1, 64))
+    dw = run_workload(wl, "cascade", repeat_check=False)
+    casc = dw.steps[0].out.float()
+    st = wl.steps[0]
+    flat_plan = spork.spork_plan_create(dw.cache, dw.shape, st.seqs, st.n_rows, [-1] * len(st.seqs))
+    info = spork.spork_plan_get_info(flat_plan)
+    assert info["unique_kv_bytes"] == info["flat_kv_bytes"]
+    img = torch.from_numpy(spork.spork_plan_image(flat_plan)).to(dw.device)
+    out = torch.empty_like(dw.steps[0].out)
+    lse = torch.empty_like(dw.steps[0].lse)
+    ws = torch.empty(info["workspace_bytes"] + 256, dtype=torch.uint8, device=dw.device)
+    spork.spork_attn_decode(flat_plan, img, dw.steps[0].q, dw.k_pool, dw.v_pool, out, lse, ws)
+    torch.cuda.synchronize()
+    diff = (out.float() - casc).abs().max().item()
+    say(f"  cascade vs flat max diff {diff:.3e}")
+    assert diff <= 2e-2
+    spork.spork_plan_destroy(flat_plan)
+    dw.close()
+
+
+def test_accept_only_mode_and_all_or_nothing_drafts():
+    wl = synth.make(3, sessions=4, prefix=64, vocab=777, verify_k=5)
+    st = wl.steps[0]
+    g = st.planted_greedy.reshape(4, 6)
+    st.drafts[0] = g[0, :5]                        # all match -> a = K, bonus token
+    st.drafts[1] = (g[1, :5] + 1) % 777            # none match -> a = 0
+    st.planted_accept[0], st.planted_next[0] = 5, g[0, 5]
+    st.planted_accept[1], st.planted_next[1] = 0, g[1, 0]
+    dw = runner.DeviceWorkload(wl)
+    step = dw.prepare(0)
+    step.poison()
+    step.run(attention=False)
+    torch.cuda.synchronize()
+    assert step.accept_len.cpu().tolist()[:2] == [5, 0]
+    assert np.array_equal(step.accept_len.cpu().numpy(), st.planted_accept)
+    assert np.array_equal(step.next_token.cpu().numpy(), st.planted_next)
+    dw.close()
