@@ -1,0 +1,266 @@
+#!/usr/bin/env python
+"""Benchmark of the forked-decode hot path on one MI355X.
+
+One step = one pass of the whole hot path over the workload's batch: the
+cascade partial attention over every fork group's shared prefix and every
+thread's private range (main decode rows, probe decode rows and the main
+threads' verify rows with the causal rule over the drafts), the log-sum-exp
+merge, the greedy argmax over the verify logits and the longest-prefix
+accept. The copy-on-write forks, appends and the plan are host work done once
+per fork, before the timed region; their host time is reported beside it.
+
+Default workload: the Qwen3-30B-A3B-shaped mixed batch (32 query / 4 KV heads,
+head dim 128, bf16, block size 16; 64 sessions x (main + 2 probes), 32768-token
+shared prefixes, log-uniform private suffixes in [1, 4096], mains verify K=8
+drafts in the same batch, vocabulary 151936), seeded synthetic data.
+
+Prints one JSON line. ``value`` is unique-KV GB/s: each shared prefix counted
+once, each private range once, over the whole step's time (inputs resident in
+HBM). ``roofline`` reports the dominant kernel (the partial attention) from
+HIP events recorded around its launches in the timed region.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "forked decode-attn unique-KV GB/s (% of 8 TB/s) + verified tokens/s"
+HBM_PEAK_GBPS = 8000.0
+DEFAULT_WORKLOAD = "qwen3-30b-a3b-mixed"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_partial_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_03333_amd", "csrc", "kernels.hip")
+
+
+def kernel_source_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the rocprofv3 counter runs, if they
+    were taken on the current kernel source for this workload."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, step_specs, target_s):
+    """The oracle, untuned, on whole sessions of the same workload until about
+    ``target_s`` seconds of CPU work; GB/s on the same unique-KV accounting."""
+    import numpy as np
+
+    import oracle
+    from paper_2607_03333_amd import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    per_tok = 2 * wl.hkv * wl.d * (2 if wl.dtype == synth.BF16 else 4)
+    sessions = sorted({t.session for t in wl.threads})
+    done, nbytes, rows, t0 = 0, 0, 0, time.perf_counter()
+    for s in sessions:
+        for si, st in step_specs:
+            row = 0
+            vrow = 0
+            for seq, n in zip(st.seqs, st.n_rows):
+                th = next(t for t in wl.threads if t.seq == seq)
+                if th.session == s:
+                    L = wl.thread_len(seq, si)
+                    k, v = wl.context(seq, L)
+                    oracle.attend(synth.to_f64(st.q[row:row + n], wl.dtype), synth.to_f64(k, wl.dtype),
+                                  synth.to_f64(v, wl.dtype), wl.sm_scale)
+                    nbytes += (L - wl.prefix_len[s]) * per_tok
+                    rows += n
+                    if st.verify_k and th.drafts:
+                        kk = st.verify_k
+                        g = oracle.argmax_rows(synth.to_f64(st.logits[vrow * (kk + 1):(vrow + 1) * (kk + 1)],
+                                                            wl.logits_dtype))
+                        oracle.accept_drafts(g, st.drafts[vrow:vrow + 1])
+                if th.drafts and st.verify_k:
+                    vrow += 1
+                row += n
+            nbytes += wl.prefix_len[s] * per_tok
+        done += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {len(sessions)} sessions ({rows} query rows, {nbytes} unique KV bytes) "
+                      f"in {dt:.1f} s, float64 NumPy, {os.cpu_count()} logical CPUs visible"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="instead of the benchmark, run one plain device copy of this many MiB "
+                         "(reference kernel for the HBM traffic counters) and exit")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the forked-decode path is "
+                                   "measured on a single MI355X; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_03333_amd import runner, spork, synth
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        sys.exit(1)
+    spork.lib()
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20)
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n}), flush=True)
+        return
+
+    t_gen = time.perf_counter()
+    wl = synth.make(args.workload)
+    print(f"# workload {wl.name}: generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
+
+    # Host work of the forks: replay the scenario's block-manager calls alone.
+    cache = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
+    t_fork = t_other = 0.0
+    for st in wl.steps:
+        for op in st.ops_before:
+            t = time.perf_counter()
+            if op[0] == "new":
+                spork.spork_seq_new(cache)
+                t_other += time.perf_counter() - t
+            elif op[0] == "append":
+                spork.spork_seq_append(cache, op[1], op[2])
+                t_other += time.perf_counter() - t
+            else:
+                spork.spork_fork(cache, op[1])
+                t_fork += time.perf_counter() - t
+    shape = spork.make_shape(wl.hq, wl.hkv, wl.d, wl.block_size,
+                             spork.SPORK_DTYPE_BF16 if wl.dtype == synth.BF16 else spork.SPORK_DTYPE_F32,
+                             wl.sm_scale)
+    t = time.perf_counter()
+    for st in wl.steps:
+        p = spork.spork_plan_create(cache, shape, st.seqs, st.n_rows, st.groups)
+        spork.spork_plan_destroy(p)
+    t_plan = time.perf_counter() - t
+    spork.spork_cache_destroy(cache)
+    n_forks = sum(1 for st in wl.steps for op in st.ops_before if op[0] == "fork")
+
+    t_setup = time.perf_counter()
+    dw = runner.DeviceWorkload(wl, poison_pool=False)
+    steps = dw.prepare_all()
+    torch.cuda.synchronize()
+    print(f"# device setup {time.perf_counter() - t_setup:.1f} s; waves {[s.info['n_waves'] for s in steps]} "
+          f"row tiles {[s.info['max_row_tiles'] for s in steps]}", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        for s in steps:
+            s.run()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spork.spork_timing_read()
+    spork.spork_timing_enable(True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        for s in steps:
+            s.run()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    spork.spork_timing_enable(False)
+    kern = spork.spork_timing_read()
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+
+    unique = sum(s.info["unique_kv_bytes"] for s in steps)
+    flat = sum(s.info["flat_kv_bytes"] for s in steps)
+    verified = 0
+    drafts_checked = 0
+    for s in steps:
+        if s.verify:
+            verified += int((s.accept_len.cpu() + 1).sum().item())
+            drafts_checked += s.n_verify * s.spec.verify_k
+    value = unique / (ms_step * 1e-3) / 1e9
+
+    attn_ms, attn_n = kern["attn_partial"]
+    attn_avg_ms = attn_ms / max(attn_n, 1)
+    attn_bytes_per_launch = unique / len(steps)
+    achieved = attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9
+    traffic = measured_traffic(wl.name)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == synth.BF16 else "f32",
+        "data": "synthetic (seeded Gaussian K/V/Q, planted greedy logits)",
+        "config": {
+            "workload": wl.name, "query_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.d,
+            "block_size": wl.block_size, "sessions": len(wl.prefix_len),
+            "threads": sum(len(s.spec.seqs) for s in steps),
+            "query_rows": sum(sum(s.spec.n_rows) for s in steps),
+            "shared_prefix_tokens": wl.prefix_len[0], "verify_k": max(s.spec.verify_k for s in steps),
+            "parallelism": "single GPU",
+        },
+        "pct_of_8TBps": round(100.0 * value / HBM_PEAK_GBPS, 2),
+        "verified_tokens_per_s": round(verified / (ms_step * 1e-3), 1) if verified else None,
+        "drafts_checked_per_s": round(drafts_checked / (ms_step * 1e-3), 1) if drafts_checked else None,
+        "unique_kv_bytes_per_step": unique,
+        "flat_kv_bytes_per_step": flat,
+        "kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items() if v[1]},
+        "host_ms": {"forks": round(t_fork * 1e3, 3), "n_forks": n_forks, "appends_and_new": round(t_other * 1e3, 3),
+                    "plan": round(t_plan * 1e3, 3)},
+        "wall_s_timed_region": round(wall, 4),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attn_partial",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "avg_launch_ms": round(attn_avg_ms, 4),
+            "algorithmic_bytes_per_launch": attn_bytes_per_launch,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, [(s.index, s.spec) for s in steps], args.cpu_seconds)
+    dw.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

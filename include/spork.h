@@ -223,6 +223,25 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
                         int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
                         void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ======================================================================== *
+ *  Kernel timing (benchmarks).
+ * ======================================================================== */
+#define SPORK_KERNEL_ATTN 0   /* cascade / private-range partial attention */
+#define SPORK_KERNEL_MERGE 1  /* log-sum-exp merge */
+#define SPORK_KERNEL_ARGMAX 2 /* greedy argmax over vocabulary chunks */
+#define SPORK_KERNEL_ACCEPT 3 /* chunk combine + longest-prefix accept */
+#define SPORK_KERNEL_KINDS 4
+
+/* While enabled (per calling thread), every hot-path call records a HIP event
+ * before and after each of its kernels on the caller's stream. */
+int spork_timing_enable(int32_t on);
+
+/* Wait for the recorded events, write the summed milliseconds and the launch
+ * count of each kernel kind into ms_out / launches_out (host arrays of
+ * SPORK_KERNEL_KINDS entries, launches_out nullable), and start a new
+ * accumulation. SPORK_E_HIP if an event cannot be read. */
+int spork_timing_read(float* ms_out, int32_t* launches_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -7,6 +7,7 @@
 #include <exception>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "block_manager.h"
 #include "kernels.h"
@@ -32,6 +33,38 @@ int fail(int code, const std::string& msg) {
 }
 
 constexpr int kAbiVersion = 1;
+
+// Per-thread kernel timing: event pairs recorded around each launch.
+struct Timing {
+  bool on = false;
+  std::vector<hipEvent_t> pool;  // created lazily, reused across reads
+  size_t used = 0;
+  std::vector<std::pair<int, size_t>> marks;  // (kind, index of the begin event)
+};
+thread_local Timing g_timing;
+
+hipEvent_t next_event() {
+  if (g_timing.used == g_timing.pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_timing.pool.push_back(e);
+  }
+  return g_timing.pool[g_timing.used++];
+}
+
+// Launch `f` on `stream`, bracketed by timing events of `kind` when enabled.
+template <typename F>
+hipError_t timed(int kind, hipStream_t stream, F&& f) {
+  if (!g_timing.on) return f();
+  const size_t at = g_timing.used;
+  hipEvent_t b = next_event(), e = next_event();
+  if (b == nullptr || e == nullptr) return hipErrorOutOfMemory;
+  hipEventRecord(b, stream);
+  const hipError_t rc = f();
+  hipEventRecord(e, stream);
+  g_timing.marks.push_back({kind, at});
+  return rc;
+}
 
 int from_bm(spork::BmStatus s, const char* what) {
   switch (s) {
@@ -227,7 +260,12 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
       return fail(SPORK_E_INVAL, "NULL argument");
     int rc = check_shape(shape);
     if (rc != SPORK_OK) return rc;
-    spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype)};
+    // bf16: 4-wave workgroups with up to 2 row tiles per wave, 2 per CU (4
+    // with 1 tile per wave); fp32: 1-wave workgroups with up to 4 row tiles,
+    // 4 per CU (8 with up to 2 tiles).
+    const bool bf16 = shape->dtype == SPORK_DTYPE_BF16;
+    spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype),
+                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 4 : 8};
     auto* plan = new spork_plan();
     plan->shape = *shape;
     const std::string err = spork::build_plan(cache->bm, ps, seqs, n_rows, groups, n_threads, n_cu, &plan->p);
@@ -312,7 +350,11 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.lse = lse;
   a.part_o = static_cast<float*>(workspace);
   a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
-  return hip_status(spork::launch_attention(a, stream), "spork_attn_decode");
+  int rc = hip_status(timed(SPORK_KERNEL_ATTN, stream, [&] { return spork::launch_attn_partial(a, stream); }),
+                      "spork_attn_decode (partial attention)");
+  if (rc != SPORK_OK) return rc;
+  return hip_status(timed(SPORK_KERNEL_MERGE, stream, [&] { return spork::launch_merge(a, stream); }),
+                    "spork_attn_decode (merge)");
 }
 
 int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
@@ -370,8 +412,39 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     a.next_token = next_token;
     a.argmax_out = argmax_out;
     a.keys = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(workspace) + att_ws);
-    return hip_status(spork::launch_accept(a, stream), "spork_verify_accept");
+    const int rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(a, stream); }),
+                              "spork_verify_accept (argmax)");
+    if (rc != SPORK_OK) return rc;
+    return hip_status(timed(SPORK_KERNEL_ACCEPT, stream, [&] { return spork::launch_accept_tail(a, stream); }),
+                      "spork_verify_accept (accept)");
   });
+}
+
+int spork_timing_enable(int32_t on) {
+  g_timing.on = on != 0;
+  return SPORK_OK;
+}
+
+int spork_timing_read(float* ms_out, int32_t* launches_out) {
+  if (ms_out == nullptr) return fail(SPORK_E_INVAL, "ms_out is NULL");
+  for (int k = 0; k < SPORK_KERNEL_KINDS; ++k) {
+    ms_out[k] = 0.0f;
+    if (launches_out) launches_out[k] = 0;
+  }
+  int rc = SPORK_OK;
+  for (const auto& m : g_timing.marks) {
+    hipEvent_t b = g_timing.pool[m.second], e = g_timing.pool[m.second + 1];
+    float ms = 0.0f;
+    if (hipEventSynchronize(e) != hipSuccess || hipEventElapsedTime(&ms, b, e) != hipSuccess) {
+      rc = fail(SPORK_E_HIP, "spork_timing_read: event not readable");
+      continue;
+    }
+    ms_out[m.first] += ms;
+    if (launches_out) launches_out[m.first] += 1;
+  }
+  g_timing.marks.clear();
+  g_timing.used = 0;
+  return rc;
 }
 
 }  // extern "C"

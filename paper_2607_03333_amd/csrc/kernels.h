@@ -31,7 +31,8 @@ struct AttnArgs {
 
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
 bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles);
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 
 struct AcceptArgs {
   const void* logits;
@@ -43,7 +44,8 @@ struct AcceptArgs {
   uint64_t* keys;  // [rows][chunks] workspace
 };
 int32_t accept_chunks(int32_t rows, int32_t vocab);
-hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream);
+hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream);
+hipError_t launch_accept_tail(const AcceptArgs& a, hipStream_t stream);
 
 hipError_t launch_kv_write(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
                            int64_t num_slots, void* k_cache, void* v_cache, const int64_t* slots,

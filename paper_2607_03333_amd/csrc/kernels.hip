@@ -19,6 +19,7 @@
 
 #include <climits>
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -99,170 +100,252 @@ __device__ __forceinline__ int wave_min_int(int x) {
 }
 
 // --------------------------------------------------------------------------
-// bf16 partial attention: RT row tiles, head dim D, block size BS.
+// bf16 partial attention. One workgroup of 4 waves owns a token range of one
+// work item and up to 4*RTW 16-row tiles of its query rows; wave w computes
+// tiles w, w+4, ... . The 32-token K/V tiles ("stages", 16 KB) are fetched
+// once per workgroup: every thread issues 4 coalesced 16-byte loads per stage,
+// kept NSTAGE_REGS stages ahead in registers, then written to one of two LDS
+// slots and shared by all waves (one barrier per stage).
 //
-// Per 32-token tile and row tile, with r16 = lane % 16 and g = lane / 16:
-//   S^T = K Q^T via v_mfma_f32_16x16x32_bf16: A-row r16 of half hh is token
-//   tb + 8*(r16/4) + 4*hh + r16%4, so the lane receives scores of query row
-//   r16 for tokens tb + 8g + j (j = 0..7, halves concatenated).
-//   O^T += V^T P^T via the same MFMA: A = V^T (channel 16*dt + r16, tokens
-//   tb + 8g .. +7: one 16-byte load from the channel-major V block),
-//   B = P^T (the lane's own 8 probabilities). The accumulator gives the lane
-//   query row r16 at channels 16*dt + 4g + i, so the rescale is lane-local.
-//   The contraction slot of channel d in Q.K is (k-step d/32, lane group
-//   (d%32)/8, element d%8) on both operands.
+// LDS slot layout (1024 chunks of 16 bytes, XOR-swizzled so that the MFMA
+// operand reads of each 8-lane group hit 8 different 128-byte bank groups):
+//   K: chunk t*16 + (c ^ fk(t)) holds channels 8c..8c+7 of tile token t,
+//      fk(t) = (t & 3) | ((t >> 1) & 4);
+//   V: chunk 512 + d*4 + (q ^ ((d >> 1) & 3)) holds tokens 8q..8q+7 of
+//      channel d (from the channel-major V blocks).
+//
+// Per stage and row tile (r16 = lane % 16, g = lane / 16 within the wave):
+//   S^T = K Q^T via v_mfma_f32_16x16x32_bf16; A-row r16 of half hh is tile
+//   token 8*(r16/4) + 4*hh + r16%4, so the lane receives scores of query row
+//   r16 for tokens 8g + j (j = 0..7, halves concatenated); the contraction
+//   slot of channel d is (k-step d/32, lane group (d%32)/8, element d%8) on
+//   both operands.
+//   O^T += V^T P^T: A = V^T (channel 16*dt + r16, tokens 8g..8g+7), B = the
+//   lane's own 8 probabilities; the accumulator holds query row r16 at
+//   channels 16*dt + 4g + i, so the rescale by the row's factor is lane-local.
 // --------------------------------------------------------------------------
-template <int RT, int D, int BS>
-__global__ void __launch_bounds__(64) attn_bf16(AttnArgs a) {
-  static_assert(D % 32 == 0 && (BS == 16 || BS == 32 || BS == 64), "unsupported shape");
-  constexpr int KS = D / 32;
-  constexpr int DT = D / 16;
+constexpr int kWgWaves = 4;
+constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 bytes / 16
+constexpr int kStageRegs = 3;       // stages in flight in registers
+
+__device__ __forceinline__ int k_swz(int t) { return (t & 3) | ((t >> 1) & 4); }
+
+struct StageRegs {
+  uint4 k0, k1, v0, v1;
+};
+
+// Zero the bf16 lanes of an 8-token chunk starting at position `first` whose
+// position is at or past `end` (two tokens per 32-bit word).
+__device__ __forceinline__ uint4 zero_past(uint4 v, int first, int end) {
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = first + 2 * i < end ? 0x0000FFFFu : 0u;
+    const uint32_t hi = first + 2 * i + 1 < end ? 0xFFFF0000u : 0u;
+    w[i] &= lo | hi;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
+
+template <int RTW, int BS>
+__global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
+  constexpr int D = 128;
+  static_assert(BS == 16 || BS == 32, "unsupported block size");
+  __shared__ uint4 smem[2][kStageChunks];
   const WaveDesc w = a.waves[blockIdx.x];
   if (w.item < 0) return;
   const ItemDesc it = a.items[w.item];
-  const int lane = threadIdx.x, r16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ qg = static_cast<const uint16_t*>(a.q);
-  const uint16_t* __restrict__ kc = static_cast<const uint16_t*>(a.k_cache);
-  const uint16_t* __restrict__ vc = static_cast<const uint16_t*>(a.v_cache);
+  const uint4* __restrict__ kc = static_cast<const uint4*>(a.k_cache);
+  const uint4* __restrict__ vc = static_cast<const uint4*>(a.v_cache);
   const int32_t* __restrict__ table = a.tables + it.table_off;
   const int nb = it.n_blocks;
   const size_t head = static_cast<size_t>(it.kv_head);
   const size_t hkv = static_cast<size_t>(a.hkv);
   const int ntiles = (w.nrows + 15) >> 4;
 
-  bf16x8 qop[RT][KS];
-  int hz[RT];
+  // Query operands and row horizons of this wave's tiles.
+  bf16x8 qop[RTW][4];
+  int hz[RTW];
+  bool own[RTW];
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int i = t * 16 + r16;
-    if (i < w.nrows) {
+  for (int j = 0; j < RTW; ++j) {
+    const int tile = wave + kWgWaves * j;
+    own[j] = tile < ntiles;
+    const int i = tile * 16 + r16;
+    if (own[j] && i < w.nrows) {
       const RowDesc rd = a.rows[it.row_off + w.row0 + i];
-      hz[t] = rd.horizon;
+      hz[j] = rd.horizon;
       const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rd.qidx) * D);
 #pragma unroll
-      for (int s = 0; s < KS; ++s) qop[t][s] = as_bf16x8(qp[4 * s + g]);
+      for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(qp[4 * s + g]);
     } else {
-      hz[t] = INT_MAX;  // padding row: zero query, never written
+      hz[j] = INT_MAX;  // padding row: zero query, never written
 #pragma unroll
-      for (int s = 0; s < KS; ++s) qop[t][s] = as_bf16x8(make_uint4(0, 0, 0, 0));
+      for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(make_uint4(0, 0, 0, 0));
     }
   }
   int hmin = INT_MAX;
 #pragma unroll
-  for (int t = 0; t < RT; ++t) hmin = min(hmin, hz[t]);
+  for (int j = 0; j < RTW; ++j) hmin = min(hmin, hz[j]);
   hmin = wave_min_int(hmin);
 
-  float m[RT], l[RT];
-  f32x4 o[RT][DT];
+  float m[RTW], l[RTW];
+  f32x4 o[RTW][8];
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    m[t] = kNegInf;
-    l[t] = 0.0f;
+  for (int j = 0; j < RTW; ++j) {
+    m[j] = kNegInf;
+    l[j] = 0.0f;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int dt = 0; dt < 8; ++dt) o[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Physical block of the tile's j-th block (clamped to the table: positions
-  // past the range are masked, and their V is zeroed before use).
-  auto blk = [&](int tb, int j) {
-    int bi = tb / BS + j;
-    bi = bi < nb ? bi : nb - 1;
-    return static_cast<size_t>(table[bi]);
+  const int tb0 = w.tok_lo & ~(kTileTokens - 1);
+  const int nstage = (w.tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
+
+  // This thread's 4 chunks of a stage: K chunks tid and tid + 256 (tile
+  // tokens tid/16 and 16 + tid/16), V chunks tid and tid + 256 (channels
+  // tid/4 and 64 + tid/4).
+  const int kt0 = tid >> 4;
+  const int kc0 = (tid & 15) ^ k_swz(kt0);
+  const int kc1 = (tid & 15) ^ k_swz(kt0 + 16);
+  const int vd0 = tid >> 2;
+  const int vq0 = (tid & 3) ^ v_swz(vd0);
+  const int vq1 = (tid & 3) ^ v_swz(vd0 + 64);
+  // Stages past the end reload the last stage (never stored): the loads stay
+  // unconditional, which keeps the register pipeline straight-line.
+  auto load_stage = [&](int st) __attribute__((always_inline)) {
+    StageRegs r;
+    const int tb = tb0 + min(st, nstage - 1) * kTileTokens;
+    int bi0 = tb / BS, bi1 = (tb + 16) / BS;
+    bi0 = bi0 < nb ? bi0 : nb - 1;
+    bi1 = bi1 < nb ? bi1 : nb - 1;
+    const size_t b0 = static_cast<size_t>(table[bi0]);
+    const size_t b1 = static_cast<size_t>(table[bi1]);
+    // K rows: token tb + t lives in block (t < 16 ? b0 : b1) at offset (tb + t) % BS
+    r.k0 = kc[((b0 * hkv + head) * BS + (tb + kt0) % BS) * (D / 8) + kc0];
+    r.k1 = kc[((b1 * hkv + head) * BS + (tb + 16 + kt0) % BS) * (D / 8) + kc1];
+    // V^T rows: tokens tb + 8q .. +7 live in block (q < 2 ? b0 : b1)
+    const size_t bv0 = vq0 < 2 ? b0 : b1;
+    const size_t bv1 = vq1 < 2 ? b0 : b1;
+    r.v0 = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(vc) +
+                                           ((bv0 * hkv + head) * D + vd0) * BS + (tb + 8 * vq0) % BS);
+    r.v1 = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(vc) +
+                                           ((bv1 * hkv + head) * D + vd0 + 64) * BS + (tb + 8 * vq1) % BS);
+    return r;
   };
-  auto load_tile = [&](int tb, bf16x8 (&kop)[2][KS], bf16x8 (&vop)[DT]) {
-    const size_t b0 = blk(tb, 0);
-    const size_t b1 = BS == 16 ? blk(tb, 1) : b0;
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int tk = 8 * (r16 >> 2) + 4 * hh + (r16 & 3);  // 0..31 within the tile
-      const size_t b = (BS == 16 && tk >= 16) ? b1 : b0;
-      const int off = (tb + tk) % BS;
-      const uint4* kp = reinterpret_cast<const uint4*>(
-          kc + ((b * hkv + head) * BS + off) * D);
-#pragma unroll
-      for (int s = 0; s < KS; ++s) kop[hh][s] = as_bf16x8(kp[4 * s + g]);
+  auto store_stage = [&](int st, StageRegs r) __attribute__((always_inline)) {
+    const int tb = tb0 + st * kTileTokens;
+    if (tb + kTileTokens > w.tok_hi) {
+      // zero V of positions past the range: they may hold anything
+      r.v0 = zero_past(r.v0, tb + 8 * vq0, w.tok_hi);
+      r.v1 = zero_past(r.v1, tb + 8 * vq1, w.tok_hi);
     }
-    const size_t bv = (BS == 16 && g >= 2) ? b1 : b0;
-    const int offv = (tb + 8 * g) % BS;
-    const uint16_t* vp = vc + (bv * hkv + head) * (static_cast<size_t>(D) * BS) + offv;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-      vop[dt] = as_bf16x8(*reinterpret_cast<const uint4*>(vp + static_cast<size_t>(16 * dt + r16) * BS));
+    uint4* slot = smem[st & 1];
+    slot[tid] = r.k0;
+    slot[tid + 256] = r.k1;
+    slot[512 + tid] = r.v0;
+    slot[512 + tid + 256] = r.v1;
   };
+
+  // Tiles this wave owns: the first `nown` of its RTW slots (wave-uniform).
+  int nown = 0;
+#pragma unroll
+  for (int j = 0; j < RTW; ++j) nown += own[j] ? 1 : 0;
 
   const float c = a.scale_log2;
-  int tb = w.tok_lo & ~(kTileTokens - 1);
-  bf16x8 kA[2][KS], vA[DT];
-  load_tile(tb, kA, vA);
-  for (; tb < w.tok_hi; tb += kTileTokens) {
-    bf16x8 kB[2][KS], vB[DT];
-    const bool more = tb + kTileTokens < w.tok_hi;
-    if (more) load_tile(tb + kTileTokens, kB, vB);
+  auto compute_tiles = [&](auto nown_c, int st) __attribute__((always_inline)) {
+    constexpr int NT = decltype(nown_c)::value;
+    const int tb = tb0 + st * kTileTokens;
+    const uint4* slot = smem[st & 1];
     const bool edge = tb < w.tok_lo || tb + kTileTokens > w.tok_hi || tb + kTileTokens - 1 > hmin;
-    if (tb + kTileTokens > w.tok_hi) {
+    f32x4 sc[NT][2];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (tb + 8 * g + j >= w.tok_hi) {
+    for (int j = 0; j < NT; ++j) sc[j][0] = sc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) vA[dt][j] = static_cast<__bf16>(0.0f);
-        }
+    for (int hh = 0; hh < 2; ++hh) {
+      const int t = 8 * (r16 >> 2) + 4 * hh + (r16 & 3);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bf16x8 kop = as_bf16x8(slot[t * 16 + ((4 * s + g) ^ k_swz(t))]);
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          sc[j][hh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[j][s], sc[j][hh], 0, 0, 0);
       }
     }
+    bf16x8 pop[NT];
+    float alpha[NT];
 #pragma unroll
-    for (int t = 0; t < RT; ++t) {
-      if (t < ntiles) {
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NT; ++j) {
+      float sv[8] = {sc[j][0][0] * c, sc[j][0][1] * c, sc[j][0][2] * c, sc[j][0][3] * c,
+                     sc[j][1][0] * c, sc[j][1][1] * c, sc[j][1][2] * c, sc[j][1][3] * c};
+      if (edge) {
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kA[0][s], qop[t][s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kA[1][s], qop[t][s], s1, 0, 0, 0);
-        }
-        float sv[8] = {s0[0] * c, s0[1] * c, s0[2] * c, s0[3] * c,
-                       s1[0] * c, s1[1] * c, s1[2] * c, s1[3] * c};
-        if (edge) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int tk = tb + 8 * g + j;
-            if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[t]) sv[j] = kNegInf;
-          }
-        }
-        const float alpha = softmax_step(sv, m[t], l[t]);
-        bf16x8 pop;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pop[j] = static_cast<__bf16>(sv[j]);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          o[t][dt] *= alpha;
-          o[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA[dt], pop, o[t][dt], 0, 0, 0);
+        for (int e = 0; e < 8; ++e) {
+          const int tk = tb + 8 * g + e;
+          if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[e] = kNegInf;
         }
       }
+      alpha[j] = softmax_step(sv, m[j], l[j]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pop[j][e] = static_cast<__bf16>(sv[e]);
     }
-    if (more) {
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
+    for (int dt = 0; dt < 8; ++dt) {
+      const int d = 16 * dt + r16;
+      const bf16x8 vop = as_bf16x8(slot[512 + d * 4 + (g ^ v_swz(d))]);
 #pragma unroll
-        for (int s = 0; s < KS; ++s) kA[hh][s] = kB[hh][s];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) vA[dt] = vB[dt];
+      for (int j = 0; j < NT; ++j) {
+        o[j][dt] *= alpha[j];
+        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[j], o[j][dt], 0, 0, 0);
+      }
     }
+  };
+  auto compute_stage = [&](int st) __attribute__((always_inline)) {
+    if (RTW >= 2 && nown == 2) compute_tiles(std::integral_constant<int, (RTW >= 2 ? 2 : 1)>{}, st);
+    else if (nown == 1) compute_tiles(std::integral_constant<int, 1>{}, st);
+  };
+
+  // Software pipeline: stages st+1 .. st+kStageRegs-1 stay in flight while
+  // stage st is written to LDS and computed.
+  StageRegs ra = load_stage(0);
+  StageRegs rb = load_stage(1);
+  for (int st = 0; st < nstage; st += kStageRegs) {
+    StageRegs rc = load_stage(st + 2);
+    store_stage(st, ra);
+    __syncthreads();
+    compute_stage(st);
+    if (st + 1 >= nstage) break;
+    ra = load_stage(st + 3);
+    store_stage(st + 1, rb);
+    __syncthreads();
+    compute_stage(st + 1);
+    if (st + 2 >= nstage) break;
+    rb = load_stage(st + 4);
+    store_stage(st + 2, rc);
+    __syncthreads();
+    compute_stage(st + 2);
   }
 
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    if (t < ntiles) {
-      float lt = l[t] + __shfl_xor(l[t], 16);
-      lt += __shfl_xor(lt, 32);
-      const int i = t * 16 + r16;
-      if (i < w.nrows) {
-        const size_t pr = static_cast<size_t>(w.partial + i);
-        if (g == 0) {
-          a.part_ml[2 * pr] = m[t];
-          a.part_ml[2 * pr + 1] = lt;
-        }
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[t][dt];
+  for (int j = 0; j < RTW; ++j) {
+    if (!own[j]) continue;
+    float lt = l[j] + __shfl_xor(l[j], 16);
+    lt += __shfl_xor(lt, 32);
+    const int i = (wave + kWgWaves * j) * 16 + r16;
+    if (i < w.nrows) {
+      const size_t pr = static_cast<size_t>(w.partial + i);
+      if (g == 0) {
+        a.part_ml[2 * pr] = m[j];
+        a.part_ml[2 * pr + 1] = lt;
       }
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+        *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[j][dt];
     }
   }
 }
@@ -608,13 +691,11 @@ __global__ void __launch_bounds__(256) kv_copy_kernel(int hkv, int D, int BS, T*
 // --------------------------------------------------------------------------
 typedef void (*AttnKernel)(AttnArgs);
 
-template <int D, int BS>
-AttnKernel pick_bf16(int rt) {
-  switch (rt) {
-    case 1: return attn_bf16<1, D, BS>;
-    case 2: return attn_bf16<2, D, BS>;
-    case 3: return attn_bf16<3, D, BS>;
-    case 4: return attn_bf16<4, D, BS>;
+template <int BS>
+AttnKernel pick_bf16(int row_tiles) {
+  switch ((row_tiles + kWgWaves - 1) / kWgWaves) {
+    case 1: return attn_bf16<1, BS>;
+    case 2: return attn_bf16<2, BS>;
     default: return nullptr;
   }
 }
@@ -632,8 +713,8 @@ AttnKernel pick_f32(int rt) {
 
 AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt) {
   if (dtype == 1 && d == 128) {
-    if (bs == 16) return pick_bf16<128, 16>(rt);
-    if (bs == 32) return pick_bf16<128, 32>(rt);
+    if (bs == 16) return pick_bf16<16>(rt);
+    if (bs == 32) return pick_bf16<32>(rt);
   }
   if (dtype == 0) {
     if (d == 64 && bs == 16) return pick_f32<64, 16>(rt);
@@ -650,23 +731,25 @@ bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, in
   return pick_attention(dtype, head_dim, block_size, row_tiles) != nullptr;
 }
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
+hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream) {
   AttnKernel k = pick_attention(a.dtype, a.head_dim, a.block_size, a.row_tiles);
   if (k == nullptr) return hipErrorInvalidValue;
-  if (a.n_waves > 0) hipLaunchKernelGGL(k, dim3(a.n_waves), dim3(64), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const int threads = a.dtype == 1 ? 64 * kWgWaves : 64;
+  if (a.n_waves > 0) hipLaunchKernelGGL(k, dim3(a.n_waves), dim3(threads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   const int blocks = (a.n_out + 3) / 4;
-  if (blocks > 0) {
-    if (a.dtype == 1 && a.head_dim == 128)
-      hipLaunchKernelGGL((merge_kernel<128, __bf16>), dim3(blocks), dim3(256), 0, stream, a);
-    else if (a.dtype == 0 && a.head_dim == 128)
-      hipLaunchKernelGGL((merge_kernel<128, float>), dim3(blocks), dim3(256), 0, stream, a);
-    else if (a.dtype == 0 && a.head_dim == 64)
-      hipLaunchKernelGGL((merge_kernel<64, float>), dim3(blocks), dim3(256), 0, stream, a);
-    else
-      return hipErrorInvalidValue;
-  }
+  if (blocks == 0) return hipSuccess;
+  if (a.dtype == 1 && a.head_dim == 128)
+    hipLaunchKernelGGL((merge_kernel<128, __bf16>), dim3(blocks), dim3(256), 0, stream, a);
+  else if (a.dtype == 0 && a.head_dim == 128)
+    hipLaunchKernelGGL((merge_kernel<128, float>), dim3(blocks), dim3(256), 0, stream, a);
+  else if (a.dtype == 0 && a.head_dim == 64)
+    hipLaunchKernelGGL((merge_kernel<64, float>), dim3(blocks), dim3(256), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -677,15 +760,18 @@ int32_t accept_chunks(int32_t rows, int32_t vocab) {
   return c < 1 ? 1 : c;
 }
 
-hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream) {
+hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream) {
   const int rows = a.n_verify * (a.k_drafts + 1);
   if (rows == 0) return hipSuccess;
   if (a.logits_dtype == 1)
     hipLaunchKernelGGL(argmax_chunks<uint16_t>, dim3(rows * a.chunks), dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL(argmax_chunks<float>, dim3(rows * a.chunks), dim3(256), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_accept_tail(const AcceptArgs& a, hipStream_t stream) {
+  if (a.n_verify == 0) return hipSuccess;
   hipLaunchKernelGGL(accept_kernel, dim3(a.n_verify), dim3(64), (a.k_drafts + 1) * sizeof(int), stream, a);
   return hipGetLastError();
 }

@@ -31,6 +31,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   if (shape.hq <= 0 || shape.hkv <= 0 || shape.hq % shape.hkv != 0)
     return "hq and hkv must be positive with hq a multiple of hkv";
   if (shape.head_dim <= 0 || shape.block_size <= 0) return "head_dim and block_size must be positive";
+  if (shape.unit_tiles_max <= 0) return "unit_tiles_max must be positive";
   if (shape.block_size != bm.block_size()) return "shape.block_size differs from the cache's block size";
   if (n_threads <= 0) return "n_threads must be positive";
   if (n_cu <= 0) n_cu = 256;
@@ -106,8 +107,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   }
 
   // Row tiles per workgroup: large row sets are split into near-equal slices
-  // of at most kMaxRowTiles tiles; every workgroup of the launch uses the
-  // largest slice size.
+  // of at most unit_tiles_max tiles; every workgroup of the launch is sized
+  // for the largest slice.
   int32_t row_tiles = 1;
   std::vector<int32_t> range_rows(ranges.size());
   for (size_t r = 0; r < ranges.size(); ++r) {
@@ -115,7 +116,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     for (int32_t t : ranges[r].threads) rows += n_rows[t] * gq;
     range_rows[r] = rows;
     const int32_t tiles = (rows + 15) / 16;
-    const int32_t slices = (tiles + kMaxRowTiles - 1) / kMaxRowTiles;
+    const int32_t slices = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
     row_tiles = std::max(row_tiles, (tiles + slices - 1) / slices);
   }
   const int32_t slice_rows = row_tiles * 16;
@@ -153,9 +154,9 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   p.n_items = static_cast<int32_t>(items.size());
 
   // Split-K: cut every item into token segments of near-equal cost so that
-  // about one full-occupancy wave of workgroups covers the batch.
-  const int32_t waves_per_cu = row_tiles <= 2 ? 8 : 4;
-  const int64_t target = static_cast<int64_t>(n_cu) * waves_per_cu;
+  // about one full-occupancy round of workgroups covers the batch.
+  const int32_t per_cu = 2 * row_tiles <= shape.unit_tiles_max ? shape.units_per_cu_half : shape.units_per_cu;
+  const int64_t target = static_cast<int64_t>(n_cu) * std::max(1, per_cu);
   int64_t cost = 0;
   for (size_t it = 0; it < items.size(); ++it) {
     const Range& rg = *item_range[it];

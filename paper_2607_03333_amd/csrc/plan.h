@@ -21,6 +21,9 @@ namespace spork {
 
 struct PlanShape {
   int32_t hq, hkv, head_dim, block_size, elem_bytes;
+  int32_t unit_tiles_max;  // 16-row tiles one attention workgroup can hold
+  int32_t units_per_cu;    // attention workgroups resident per compute unit
+  int32_t units_per_cu_half;  // the same when every workgroup needs at most half the tiles
 };
 
 struct Plan {

@@ -6,6 +6,7 @@ namespace spork {
 
 // One attention workgroup: a token range of one work item and a slice of the
 // item's query rows. item < 0 marks a padding workgroup that exits at once.
+// (The bf16 kernel runs a workgroup as 4 waves, the fp32 kernel as 1.)
 struct WaveDesc {
   int32_t item;
   int32_t tok_lo;   // first context position of the range
@@ -33,7 +34,6 @@ struct RowDesc {
 };
 
 constexpr int kTileTokens = 32;   // tokens per inner-loop tile
-constexpr int kMaxRowTiles = 4;   // 16-row MFMA tiles per workgroup (register budget)
 constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, workgroups dealt round-robin
 
 }  // namespace spork

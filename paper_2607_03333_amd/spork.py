@@ -23,6 +23,12 @@ SPORK_E_CAPACITY = -4
 SPORK_E_HIP = -5
 SPORK_DTYPE_F32 = 0
 SPORK_DTYPE_BF16 = 1
+SPORK_KERNEL_ATTN = 0
+SPORK_KERNEL_MERGE = 1
+SPORK_KERNEL_ARGMAX = 2
+SPORK_KERNEL_ACCEPT = 3
+SPORK_KERNEL_KINDS = 4
+KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept")
 
 _c_i32 = ctypes.c_int32
 _c_i64 = ctypes.c_int64
@@ -79,6 +85,8 @@ _SIGNATURES = {
                                                     ctypes.POINTER(ctypes.c_size_t)]),
     "spork_verify_accept": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _c_i32, _c_i32, _p,
                                            _c_i32, _c_i32, _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "spork_timing_enable": (ctypes.c_int, [_c_i32]),
+    "spork_timing_read": (ctypes.c_int, [_p, _p]),
 }
 
 _lib = None
@@ -271,3 +279,16 @@ def spork_verify_accept(plan, dev_image, q, k_cache, v_cache, out, lse, logits, 
                                      _ptr(drafts), n_verify, k_drafts, _ptr(accept_len),
                                      _ptr(next_token), _ptr(argmax_out), _ptr(workspace), ws_bytes,
                                      _stream(stream)))
+
+
+# ---- kernel timing ------------------------------------------------------------
+def spork_timing_enable(on):
+    _check(lib().spork_timing_enable(1 if on else 0))
+
+
+def spork_timing_read():
+    """{kernel name: (total ms, launches)} since the last read."""
+    ms = np.zeros(SPORK_KERNEL_KINDS, dtype=np.float32)
+    n = np.zeros(SPORK_KERNEL_KINDS, dtype=np.int32)
+    _check(lib().spork_timing_read(_ptr(ms), _ptr(n)))
+    return {KERNEL_NAMES[k]: (float(ms[k]), int(n[k])) for k in range(SPORK_KERNEL_KINDS)}
