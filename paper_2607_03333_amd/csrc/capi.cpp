@@ -260,12 +260,12 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
       return fail(SPORK_E_INVAL, "NULL argument");
     int rc = check_shape(shape);
     if (rc != SPORK_OK) return rc;
-    // bf16: 4-wave workgroups with up to 2 row tiles per wave, 2 per CU (4
-    // with 1 tile per wave); fp32: 1-wave workgroups with up to 4 row tiles,
+    // bf16: 4-wave workgroups with up to 2 row tiles per wave, 2 per CU
+    // (their 68 KB of LDS); fp32: 1-wave workgroups with up to 4 row tiles,
     // 4 per CU (8 with up to 2 tiles).
     const bool bf16 = shape->dtype == SPORK_DTYPE_BF16;
     spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype),
-                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 4 : 8};
+                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 2 : 8};
     auto* plan = new spork_plan();
     plan->shape = *shape;
     const std::string err = spork::build_plan(cache->bm, ps, seqs, n_rows, groups, n_threads, n_cu, &plan->p);

@@ -102,10 +102,13 @@ __device__ __forceinline__ int wave_min_int(int x) {
 // --------------------------------------------------------------------------
 // bf16 partial attention. One workgroup of 4 waves owns a token range of one
 // work item and up to 4*RTW 16-row tiles of its query rows; wave w computes
-// tiles w, w+4, ... . The 32-token K/V tiles ("stages", 16 KB) are fetched
-// once per workgroup: every thread issues 4 coalesced 16-byte loads per stage,
-// kept NSTAGE_REGS stages ahead in registers, then written to one of two LDS
-// slots and shared by all waves (one barrier per stage).
+// tiles w, w+4, ... . The range streams through a ring of kRing LDS slots, one
+// 32-token K/V tile ("stage", 16 KB) each, filled by direct global-to-LDS
+// 16-byte loads (global_load_lds_dwordx4: lane i of an instruction lands at
+// the instruction's LDS base + 16*i), so kRing-1 stages stay in flight without
+// holding registers. Each wave issues 4 such loads per stage (waves 0-1 the K
+// half, waves 2-3 the V half); one barrier per stage publishes a slot to all
+// waves and frees the slot read in the previous stage.
 //
 // LDS slot layout (1024 chunks of 16 bytes, XOR-swizzled so that the MFMA
 // operand reads of each 8-lane group hit 8 different 128-byte bank groups):
@@ -126,13 +129,15 @@ __device__ __forceinline__ int wave_min_int(int x) {
 // --------------------------------------------------------------------------
 constexpr int kWgWaves = 4;
 constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 bytes / 16
-constexpr int kStageRegs = 3;       // stages in flight in registers
+constexpr int kRing = 4;            // LDS stages per workgroup (kRing - 1 in flight)
+constexpr int kUnitBlocks = 1040;   // block-table entries a unit may span (see kMaxUnitTokens)
+constexpr float kRescaleSlack = 8.0f;  // base-2 headroom before the reference max moves
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* global_void_ptr;
 
 __device__ __forceinline__ int k_swz(int t) { return (t & 3) | ((t >> 1) & 4); }
-
-struct StageRegs {
-  uint4 k0, k1, v0, v1;
-};
+__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
 
 // Zero the bf16 lanes of an 8-token chunk starting at position `first` whose
 // position is at or past `end` (two tokens per 32-bit word).
@@ -146,13 +151,61 @@ __device__ __forceinline__ uint4 zero_past(uint4 v, int first, int end) {
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
-__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
+
+// LDS operand reads outside the compiler's view. The compiler cannot tell the
+// direct-to-LDS loads of later stages from these reads of the current stage
+// and would otherwise wait for every load in flight before each read. The
+// waits are explicit: lds_wait() takes the destination registers as in-out
+// operands, so no consumer can be scheduled before it.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_ptr)(const_cast<void*>(p))));
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+  return r;
+}
+
+// One dword from LDS at a wave-uniform address, returned in an SGPR.
+__device__ __forceinline__ int lds_read_uniform_i32(uint32_t addr) {
+  int r;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(addr) : "memory");
+  return __builtin_amdgcn_readfirstlane(r);
+}
+
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4 (&r)[N]) {
+  static_assert(N == 8, "lds_wait expects 8 registers");
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]),
+                 "+v"(r[7])
+               :
+               : "memory");
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): callers make
+// their own direct-to-LDS loads complete first (wait_vmcnt). The memory
+// clobber keeps loads, stores and LDS operations on their side of it.
+__device__ __forceinline__ void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt on the vector-memory counter only (expcnt and lgkmcnt left open).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 template <int RTW, int BS>
 __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   constexpr int D = 128;
   static_assert(BS == 16 || BS == 32, "unsupported block size");
-  __shared__ uint4 smem[2][kStageChunks];
+  __shared__ uint4 smem[kRing][kStageChunks];
+  __shared__ int tab[kUnitBlocks];
   const WaveDesc w = a.waves[blockIdx.x];
   if (w.item < 0) return;
   const ItemDesc it = a.items[w.item];
@@ -160,8 +213,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ qg = static_cast<const uint16_t*>(a.q);
-  const uint4* __restrict__ kc = static_cast<const uint4*>(a.k_cache);
-  const uint4* __restrict__ vc = static_cast<const uint4*>(a.v_cache);
+  const uint16_t* __restrict__ kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* __restrict__ vc = static_cast<const uint16_t*>(a.v_cache);
   const int32_t* __restrict__ table = a.tables + it.table_off;
   const int nb = it.n_blocks;
   const size_t head = static_cast<size_t>(it.kv_head);
@@ -193,6 +246,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < RTW; ++j) hmin = min(hmin, hz[j]);
   hmin = wave_min_int(hmin);
+  int nown = 0;  // tiles this wave owns: the first `nown` of its RTW slots
+#pragma unroll
+  for (int j = 0; j < RTW; ++j) nown += own[j] ? 1 : 0;
 
   float m[RTW], l[RTW];
   f32x4 o[RTW][8];
@@ -207,82 +263,116 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   const int tb0 = w.tok_lo & ~(kTileTokens - 1);
   const int nstage = (w.tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
 
-  // This thread's 4 chunks of a stage: K chunks tid and tid + 256 (tile
-  // tokens tid/16 and 16 + tid/16), V chunks tid and tid + 256 (channels
-  // tid/4 and 64 + tid/4).
-  const int kt0 = tid >> 4;
-  const int kc0 = (tid & 15) ^ k_swz(kt0);
-  const int kc1 = (tid & 15) ^ k_swz(kt0 + 16);
-  const int vd0 = tid >> 2;
-  const int vq0 = (tid & 3) ^ v_swz(vd0);
-  const int vq1 = (tid & 3) ^ v_swz(vd0 + 64);
-  // Stages past the end reload the last stage (never stored): the loads stay
-  // unconditional, which keeps the register pipeline straight-line.
-  auto load_stage = [&](int st) __attribute__((always_inline)) {
-    StageRegs r;
-    const int tb = tb0 + min(st, nstage - 1) * kTileTokens;
-    int bi0 = tb / BS, bi1 = (tb + 16) / BS;
-    bi0 = bi0 < nb ? bi0 : nb - 1;
-    bi1 = bi1 < nb ? bi1 : nb - 1;
-    const size_t b0 = static_cast<size_t>(table[bi0]);
-    const size_t b1 = static_cast<size_t>(table[bi1]);
-    // K rows: token tb + t lives in block (t < 16 ? b0 : b1) at offset (tb + t) % BS
-    r.k0 = kc[((b0 * hkv + head) * BS + (tb + kt0) % BS) * (D / 8) + kc0];
-    r.k1 = kc[((b1 * hkv + head) * BS + (tb + 16 + kt0) % BS) * (D / 8) + kc1];
-    // V^T rows: tokens tb + 8q .. +7 live in block (q < 2 ? b0 : b1)
-    const size_t bv0 = vq0 < 2 ? b0 : b1;
-    const size_t bv1 = vq1 < 2 ? b0 : b1;
-    r.v0 = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(vc) +
-                                           ((bv0 * hkv + head) * D + vd0) * BS + (tb + 8 * vq0) % BS);
-    r.v1 = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(vc) +
-                                           ((bv1 * hkv + head) * D + vd0 + 64) * BS + (tb + 8 * vq1) % BS);
-    return r;
-  };
-  auto store_stage = [&](int st, StageRegs r) __attribute__((always_inline)) {
-    const int tb = tb0 + st * kTileTokens;
-    if (tb + kTileTokens > w.tok_hi) {
-      // zero V of positions past the range: they may hold anything
-      r.v0 = zero_past(r.v0, tb + 8 * vq0, w.tok_hi);
-      r.v1 = zero_past(r.v1, tb + 8 * vq1, w.tok_hi);
-    }
-    uint4* slot = smem[st & 1];
-    slot[tid] = r.k0;
-    slot[tid + 256] = r.k1;
-    slot[512 + tid] = r.v0;
-    slot[512 + tid + 256] = r.v1;
-  };
-
-  // Tiles this wave owns: the first `nown` of its RTW slots (wave-uniform).
-  int nown = 0;
+  // This lane's 4 chunks of a stage: instruction k of wave w fills chunks
+  // (4w + k)*64 + lane. Waves 0-1: K chunks (token t, channel group c);
+  // waves 2-3: V chunks (channel d, token octet q). The element offset inside
+  // a block and the block (first or second of the stage) are fixed per lane.
+  size_t off[4];
+  bool second[4];
 #pragma unroll
-  for (int j = 0; j < RTW; ++j) nown += own[j] ? 1 : 0;
-
-  const float c = a.scale_log2;
-  auto compute_tiles = [&](auto nown_c, int st) __attribute__((always_inline)) {
-    constexpr int NT = decltype(nown_c)::value;
+  for (int k = 0; k < 4; ++k) {
+    const int chunk = (4 * wave + k) * 64 + lane;
+    if (wave < 2) {
+      const int t = chunk >> 4;
+      const int cg = (chunk & 15) ^ k_swz(t);
+      second[k] = BS == 16 && t >= 16;
+      off[k] = static_cast<size_t>(t % BS) * D + 8 * cg;
+    } else {
+      const int d = (chunk - 512) >> 2;
+      const int q = (chunk & 3) ^ v_swz(d);
+      second[k] = BS == 16 && q >= 2;
+      off[k] = static_cast<size_t>(d) * BS + (8 * q) % BS;
+    }
+  }
+  const uint16_t* pool = wave < 2 ? kc : vc;
+  static_assert(kRing - 2 == 2, "the vmcnt ladder below assumes two stages in flight behind the current one");
+  // The unit's slice of the block table, staged in LDS before the ring
+  // starts (tab[i] = table entry tb0/BS + i, clamped to the table) and read
+  // per stage outside the compiler's view (a vector load of the table inside
+  // the loop would make its wait also wait for every direct-to-LDS load
+  // issued before it).
+  const int tab0 = tb0 / BS;
+  const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
+  for (int i = tid; i < ntab; i += 256) {
+    const int bi = tab0 + i;
+    tab[i] = table[bi < nb ? bi : nb - 1];
+  }
+  __syncthreads();
+  // Issue the direct-to-LDS loads of stage `st` into ring slot st % kRing.
+  auto issue_stage = [&](int st) __attribute__((always_inline)) {
     const int tb = tb0 + st * kTileTokens;
-    const uint4* slot = smem[st & 1];
+    const int e0 = lds_read_uniform_i32(lds_addr(&tab[tb / BS - tab0]));
+    const int e1 = lds_read_uniform_i32(lds_addr(&tab[(tb + 16) / BS - tab0]));
+    const size_t base0 = (static_cast<size_t>(e0) * hkv + head) * (static_cast<size_t>(BS) * D);
+    const size_t base1 = (static_cast<size_t>(e1) * hkv + head) * (static_cast<size_t>(BS) * D);
+    uint4* slot = smem[st % kRing];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint16_t* src = pool + (second[k] ? base1 : base0) + off[k];
+      __builtin_amdgcn_global_load_lds((global_void_ptr)src, (lds_void_ptr)(slot + (4 * wave + k) * 64), 16, 0, 0);
+    }
+  };
+
+  // Per-lane LDS byte addresses of the MFMA operands inside ring slot 0
+  // (slot k adds k * 16 KB as an immediate offset):
+  //   K operand (half hh, k-step s): token t = 8*(r16/4) + 4*hh + r16%4,
+  //     chunk t*16 + ((4s + g) ^ fk(t));
+  //   V operand (channel tile dt): chunk 512 + 4*(16*dt + r16) + (g ^ ((r16 >> 1) & 3)),
+  //     i.e. a per-lane base plus 1024 bytes per dt.
+  uint32_t kaddr[8];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int t = 8 * (r16 >> 2) + 4 * hh + (r16 & 3);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kaddr[4 * hh + s] = 16u * (t * 16 + ((4 * s + g) ^ k_swz(t)));
+  }
+  const uint32_t smem_base = lds_addr(&smem[0][0]);
+  const uint32_t vaddr = smem_base + 16u * (512 + 4 * r16 + (g ^ ((r16 >> 1) & 3)));
+#pragma unroll
+  for (int i = 0; i < 8; ++i) kaddr[i] += smem_base;
+
+  // Softmax in base 2 with a lazily moved reference max: scores enter as
+  // p = 2^(s*c - m) with m the row's reference; m (and the accumulator, by
+  // 2^(m_old - m_new)) moves only when a score exceeds m + kRescaleSlack, so
+  // p <= 2^kRescaleSlack and most stages skip the rescale. The merge only
+  // needs (m, l, o) to be consistent, not m to be the exact maximum.
+  const float c = a.scale_log2;
+  // One stage for NT owned tiles, reading ring slot (st % kRing).
+  auto compute_tiles = [&](auto nt_c, int st) __attribute__((always_inline)) {
+    constexpr int NT = decltype(nt_c)::value;
+    const int tb = tb0 + st * kTileTokens;
+    const uint32_t soff = static_cast<uint32_t>(st % kRing) * (kStageChunks * 16);
     const bool edge = tb < w.tok_lo || tb + kTileTokens > w.tok_hi || tb + kTileTokens - 1 > hmin;
+    u32x4 kr[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) kr[i] = lds_read_b128(kaddr[i] + soff);
+    lds_wait(kr);
     f32x4 sc[NT][2];
 #pragma unroll
     for (int j = 0; j < NT; ++j) sc[j][0] = sc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int t = 8 * (r16 >> 2) + 4 * hh + (r16 & 3);
+    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const bf16x8 kop = as_bf16x8(slot[t * 16 + ((4 * s + g) ^ k_swz(t))]);
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int j = 0; j < NT; ++j)
-          sc[j][hh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[j][s], sc[j][hh], 0, 0, 0);
-      }
-    }
+          sc[j][hh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[4 * hh + s]),
+                                                               qop[j][s], sc[j][hh], 0, 0, 0);
+    const uint32_t va = vaddr + soff;
+    u32x4 vr[8];
+    vr[0] = lds_read_b128<0 * 1024>(va);
+    vr[1] = lds_read_b128<1 * 1024>(va);
+    vr[2] = lds_read_b128<2 * 1024>(va);
+    vr[3] = lds_read_b128<3 * 1024>(va);
+    vr[4] = lds_read_b128<4 * 1024>(va);
+    vr[5] = lds_read_b128<5 * 1024>(va);
+    vr[6] = lds_read_b128<6 * 1024>(va);
+    vr[7] = lds_read_b128<7 * 1024>(va);
     bf16x8 pop[NT];
-    float alpha[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-      float sv[8] = {sc[j][0][0] * c, sc[j][0][1] * c, sc[j][0][2] * c, sc[j][0][3] * c,
-                     sc[j][1][0] * c, sc[j][1][1] * c, sc[j][1][2] * c, sc[j][1][3] * c};
+      float sv[8] = {sc[j][0][0], sc[j][0][1], sc[j][0][2], sc[j][0][3],
+                     sc[j][1][0], sc[j][1][1], sc[j][1][2], sc[j][1][3]};
       if (edge) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -290,64 +380,96 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
           if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[e] = kNegInf;
         }
       }
-      alpha[j] = softmax_step(sv, m[j], l[j]);
+      // Common case: every score is within kRescaleSlack of the row's
+      // reference, checked lane by lane; only when some lane of the wave sees
+      // a larger score are the row maxima reduced across lanes and the
+      // reference moved (rows that did not trigger keep theirs).
+      float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])), fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+      mx *= c;
+      if (__ballot(mx > m[j] + kRescaleSlack) != 0) {
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (mx > m[j] + kRescaleSlack) {  // row-uniform: all 4 lanes of the row agree
+          const float alpha = exp2_fast(m[j] - mx);  // 0 for a row's first visible tile
+          l[j] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[j][dt] *= alpha;
+          m[j] = mx;
+        }
+      }
+      const float mu = m[j] == kNegInf ? 0.0f : m[j];
+      float ps = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
+        ps += sv[e];
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) pop[j][e] = static_cast<__bf16>(sv[e]);
+      l[j] += ps;
+    }
+    lds_wait(vr);
+    if (tb + kTileTokens > w.tok_hi) {
+      // positions past the range may hold anything: zero their V (0 * NaN
+      // would poison the accumulator)
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        const uint4 z = zero_past(make_uint4(vr[dt][0], vr[dt][1], vr[dt][2], vr[dt][3]), tb + 8 * g, w.tok_hi);
+        vr[dt] = u32x4{z.x, z.y, z.z, z.w};
+      }
     }
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const int d = 16 * dt + r16;
-      const bf16x8 vop = as_bf16x8(slot[512 + d * 4 + (g ^ v_swz(d))]);
+    for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        o[j][dt] *= alpha[j];
-        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[j], o[j][dt], 0, 0, 0);
+      for (int j = 0; j < NT; ++j)
+        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[dt]), pop[j], o[j][dt], 0,
+                                                           0, 0);
+  };
+
+  // Everything loaded so far (query rows) completes before the ring starts,
+  // so no wait for it lands inside the loop.
+  wait_vmcnt<0>();
+  // Prologue: stages 0 .. kRing-2 in flight.
+#pragma unroll
+  for (int st = 0; st < kRing - 1; ++st)
+    if (st < nstage) issue_stage(st);
+
+  // The ring loop, specialised on the number of tiles this wave owns so that
+  // no branch on it sits inside the loop. Every wave runs nstage barriers.
+  auto run = [&](auto nt_c) __attribute__((always_inline)) {
+    constexpr int NT = decltype(nt_c)::value;
+    for (int st = 0; st < nstage; ++st) {
+      // Wait for this wave's loads of stage st: the stages issued after it
+      // (at most kRing - 2 of them, 4 loads each) may stay in flight.
+      const int after = min(kRing - 2, nstage - 1 - st);
+      if (after >= 2) wait_vmcnt<8>();
+      else if (after == 1) wait_vmcnt<4>();
+      else wait_vmcnt<0>();
+      barrier_nofence();  // stage st visible to all waves; slot of stage st-1 free
+      if (st + kRing - 1 < nstage) issue_stage(st + kRing - 1);
+      if constexpr (NT > 0) compute_tiles(nt_c, st);
+    }
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      float lt = l[j] + __shfl_xor(l[j], 16);
+      lt += __shfl_xor(lt, 32);
+      const int i = (wave + kWgWaves * j) * 16 + r16;
+      if (i < w.nrows) {
+        const size_t pr = static_cast<size_t>(w.partial + i);
+        if (g == 0) {
+          a.part_ml[2 * pr] = m[j];
+          a.part_ml[2 * pr + 1] = lt;
+        }
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt)
+          *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[j][dt];
       }
     }
   };
-  auto compute_stage = [&](int st) __attribute__((always_inline)) {
-    if (RTW >= 2 && nown == 2) compute_tiles(std::integral_constant<int, (RTW >= 2 ? 2 : 1)>{}, st);
-    else if (nown == 1) compute_tiles(std::integral_constant<int, 1>{}, st);
-  };
-
-  // Software pipeline: stages st+1 .. st+kStageRegs-1 stay in flight while
-  // stage st is written to LDS and computed.
-  StageRegs ra = load_stage(0);
-  StageRegs rb = load_stage(1);
-  for (int st = 0; st < nstage; st += kStageRegs) {
-    StageRegs rc = load_stage(st + 2);
-    store_stage(st, ra);
-    __syncthreads();
-    compute_stage(st);
-    if (st + 1 >= nstage) break;
-    ra = load_stage(st + 3);
-    store_stage(st + 1, rb);
-    __syncthreads();
-    compute_stage(st + 1);
-    if (st + 2 >= nstage) break;
-    rb = load_stage(st + 4);
-    store_stage(st + 2, rc);
-    __syncthreads();
-    compute_stage(st + 2);
-  }
-
-#pragma unroll
-  for (int j = 0; j < RTW; ++j) {
-    if (!own[j]) continue;
-    float lt = l[j] + __shfl_xor(l[j], 16);
-    lt += __shfl_xor(lt, 32);
-    const int i = (wave + kWgWaves * j) * 16 + r16;
-    if (i < w.nrows) {
-      const size_t pr = static_cast<size_t>(w.partial + i);
-      if (g == 0) {
-        a.part_ml[2 * pr] = m[j];
-        a.part_ml[2 * pr + 1] = lt;
-      }
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
-        *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[j][dt];
-    }
-  }
+  if (RTW >= 2 && nown == 2) run(std::integral_constant<int, (RTW >= 2 ? 2 : 1)>{});
+  else if (nown == 1) run(std::integral_constant<int, 1>{});
+  else run(std::integral_constant<int, 0>{});
 }
 
 // --------------------------------------------------------------------------

@@ -163,23 +163,31 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
     cost += static_cast<int64_t>(rg.hi - rg.lo) * slices;
   }
-  int64_t seg = (cost + target - 1) / target;
-  seg = std::max<int64_t>(kTileTokens, (seg + kTileTokens - 1) / kTileTokens * kTileTokens);
+  // Ideal tokens per workgroup slot; each item is cut into round(len / ideal)
+  // pieces (at least 1, at most kMaxUnitTokens long) so that equal items fill
+  // whole rounds of the resident workgroups.
+  const double ideal = std::max(1.0, static_cast<double>(cost) / static_cast<double>(target));
 
   std::vector<Unit> units;
   for (size_t it = 0; it < items.size(); ++it) {
     const Range& rg = *item_range[it];
     const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
     const int64_t n = rg.hi - rg.lo;
-    const int64_t nseg = std::max<int64_t>(1, (n + seg - 1) / seg);
+    int64_t nseg = std::max<int64_t>(1, static_cast<int64_t>(static_cast<double>(n) / ideal + 0.5));
+    nseg = std::max<int64_t>(nseg, (n + kMaxUnitTokens - 1) / kMaxUnitTokens);
+    nseg = std::min<int64_t>(nseg, std::max<int64_t>(1, n / kTileTokens));
     int32_t lo = rg.lo;
     for (int64_t k = 1; k <= nseg; ++k) {
       int32_t hi = rg.hi;
       if (k < nseg) {
         const int64_t cut = rg.lo + n * k / nseg;
-        hi = static_cast<int32_t>(cut / kTileTokens * kTileTokens);
-        if (hi <= lo) continue;
+        hi = static_cast<int32_t>((cut + kTileTokens / 2) / kTileTokens * kTileTokens);
+        if (hi <= lo || hi >= rg.hi) continue;
       }
+      // block-table span the kernel stages for this unit (kernel tables hold 1040)
+      const int32_t tb0 = lo / kTileTokens * kTileTokens;
+      const int32_t span_end = tb0 + (hi - tb0 + kTileTokens - 1) / kTileTokens * kTileTokens + 16;
+      if (span_end / shape.block_size - tb0 / shape.block_size + 1 > 1040) return "internal: unit too long";
       units.push_back({static_cast<int32_t>(it), lo, hi, slices});
       lo = hi;
     }

@@ -34,6 +34,10 @@ struct RowDesc {
 };
 
 constexpr int kTileTokens = 32;   // tokens per inner-loop tile
+// Longest token range of one work unit: its block-table slice (at most
+// (kMaxUnitTokens + 3 * 32) / 16 + 1 entries for 16-token blocks) is staged
+// in a 1040-entry LDS table by the bf16 kernel.
+constexpr int kMaxUnitTokens = 16384;
 constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, workgroups dealt round-robin
 
 }  // namespace spork
