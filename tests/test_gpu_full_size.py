@@ -1,0 +1,51 @@
+"""GPU parity at the workloads' full sizes, in the configuration bench.py times.
+
+The whole batch runs through the C ABI; the oracle recomputes a sample of
+threads one by one (the first and last thread, the longest context, the
+shortest private range, and a verify thread where there is one), element by
+element. Argmax and accept are compared on every row, bit-exactly, against
+the oracle and against the generator's planted values.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_03333_amd import runner, synth
+from gpu_cases import compare_accept, compare_attention, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _pick(wl, step_index):
+    st = wl.steps[step_index]
+    n = len(st.seqs)
+    lens = [wl.thread_len(s, step_index) for s in st.seqs]
+    priv = [L - wl.prefix_len[next(t.session for t in wl.threads if t.seq == s)] for s, L in zip(st.seqs, lens)]
+    pick = {0, n // 2, n - 1, int(np.argmax(lens)), int(np.argmin(priv))}
+    verify = [i for i, r in enumerate(st.n_rows) if r > 1]
+    if verify:
+        pick.add(verify[-1])
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("index", [0, 1, 2, 3, 4])
+def test_full_size_workload(index):
+    wl = synth.make(index)
+    say(f"[full {wl.name}] generated; blocks {wl.num_blocks}")
+    dw = runner.DeviceWorkload(wl, poison_pool=True)
+    try:
+        steps = dw.prepare_all()
+        assert int(dw.bad_slots.item()) == 0
+        for step in steps:
+            step.poison()
+            step.run()
+            torch.cuda.synchronize()
+            pick = _pick(wl, step.index)
+            say(f"[full {wl.name}] step {step.index}: {step.info['n_waves']} workgroups, checking threads {pick}")
+            compare_attention(wl, step, set(pick), tag=f"full {wl.name} step {step.index}")
+            out = step.out.float()
+            assert bool(torch.isfinite(out).all()), "non-finite outputs"
+            if step.verify:
+                compare_accept(wl, step, tag=f"full {wl.name} step {step.index}")
+    finally:
+        dw.close()
