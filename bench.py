@@ -210,6 +210,7 @@ def main():
 
     attn_ms, attn_n = kern["attn_partial"]
     attn_avg_ms = attn_ms / max(attn_n, 1)
+    logits_bytes = sum(s.logits.numel() * s.logits.element_size() for s in steps if s.verify)
     attn_bytes_per_launch = unique / len(steps)
     achieved = attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9
     traffic = measured_traffic(wl.name)
@@ -239,6 +240,7 @@ def main():
         "verified_tokens_per_s": round(verified / (ms_step * 1e-3), 1) if verified else None,
         "drafts_checked_per_s": round(drafts_checked / (ms_step * 1e-3), 1) if drafts_checked else None,
         "unique_kv_bytes_per_step": unique,
+        "logits_bytes_per_step": logits_bytes,
         "flat_kv_bytes_per_step": flat,
         "kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items() if v[1]},
         "host_ms": {"forks": round(t_fork * 1e3, 3), "n_forks": n_forks, "appends_and_new": round(t_other * 1e3, 3),

@@ -215,7 +215,9 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
  * argmax_out[n_verify*(k_drafts+1)] (nullable) = every row's greedy token.
  * Ties pick the lowest vocabulary index; logits must be finite.
  * workspace: the attention's workspace followed (at a 256-byte aligned
- * offset) by spork_verify_workspace_bytes; ws_bytes covers both. */
+ * offset) by spork_verify_workspace_bytes; ws_bytes covers both.
+ * With a plan the step is three launches on `stream`: partial attention,
+ * argmax, then the merge together with the accept. */
 int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q,
                         const void* k_cache, const void* v_cache, void* out, float* lse,
                         const void* logits, int32_t logits_dtype, int32_t vocab,
@@ -227,9 +229,9 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
  *  Kernel timing (benchmarks).
  * ======================================================================== */
 #define SPORK_KERNEL_ATTN 0   /* cascade / private-range partial attention */
-#define SPORK_KERNEL_MERGE 1  /* log-sum-exp merge */
+#define SPORK_KERNEL_MERGE 1  /* log-sum-exp merge (+ the verify step's accept) */
 #define SPORK_KERNEL_ARGMAX 2 /* greedy argmax over vocabulary chunks */
-#define SPORK_KERNEL_ACCEPT 3 /* chunk combine + longest-prefix accept */
+#define SPORK_KERNEL_ACCEPT 3 /* accept of an accept-only call (plan == NULL) */
 #define SPORK_KERNEL_KINDS 4
 
 /* While enabled (per calling thread), every hot-path call records a HIP event

@@ -311,9 +311,11 @@ int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap) {
   return SPORK_OK;
 }
 
+// Attention over a plan; with `acc` (a verify step) the argmax runs after the
+// attention and the accept rides in the merge launch.
 static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
                      const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
-                     hipStream_t stream) {
+                     const spork::AcceptArgs* acc, hipStream_t stream) {
   const spork::Plan& p = plan->p;
   const spork_shape& sh = plan->shape;
   if (!spork::attention_supported(sh.dtype, sh.head_dim, sh.block_size, p.row_tiles))
@@ -350,9 +352,16 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.lse = lse;
   a.part_o = static_cast<float*>(workspace);
   a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
+  const bool verify = acc != nullptr && acc->n_verify > 0;
+  if (verify) a.acc = *acc;
   int rc = hip_status(timed(SPORK_KERNEL_ATTN, stream, [&] { return spork::launch_attn_partial(a, stream); }),
                       "spork_attn_decode (partial attention)");
   if (rc != SPORK_OK) return rc;
+  if (verify) {
+    rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(*acc, stream); }),
+                    "spork_verify_accept (argmax)");
+    if (rc != SPORK_OK) return rc;
+  }
   return hip_status(timed(SPORK_KERNEL_MERGE, stream, [&] { return spork::launch_merge(a, stream); }),
                     "spork_attn_decode (merge)");
 }
@@ -362,7 +371,7 @@ int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void*
                       hipStream_t stream) {
   return guarded([&] {
     if (plan == nullptr) return fail(SPORK_E_INVAL, "plan is NULL");
-    return attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, stream);
+    return attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, nullptr, stream);
   });
 }
 
@@ -395,11 +404,6 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     if (ws_bytes < att_ws + acc_ws) return fail(SPORK_E_CAPACITY, "workspace too small for attention + accept");
     if ((att_ws + acc_ws) > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
       return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
-    if (plan != nullptr) {
-      const int rc = attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, stream);
-      if (rc != SPORK_OK) return rc;
-    }
-    if (n_verify == 0) return SPORK_OK;
     spork::AcceptArgs a{};
     a.logits = logits;
     a.logits_dtype = logits_dtype;
@@ -412,6 +416,9 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     a.next_token = next_token;
     a.argmax_out = argmax_out;
     a.keys = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(workspace) + att_ws);
+    if (plan != nullptr)
+      return attention(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, ws_bytes, &a, stream);
+    if (n_verify == 0) return SPORK_OK;
     const int rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(a, stream); }),
                               "spork_verify_accept (argmax)");
     if (rc != SPORK_OK) return rc;

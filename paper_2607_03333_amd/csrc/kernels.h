@@ -10,6 +10,16 @@
 
 namespace spork {
 
+struct AcceptArgs {
+  const void* logits;
+  int32_t logits_dtype, vocab, n_verify, k_drafts, chunks;
+  const int32_t* drafts;
+  int32_t* accept_len;
+  int32_t* next_token;
+  int32_t* argmax_out;
+  uint64_t* keys;  // [rows][chunks] workspace
+};
+
 struct AttnArgs {
   const WaveDesc* waves;
   const ItemDesc* items;
@@ -27,22 +37,17 @@ struct AttnArgs {
   float* lse;
   float* part_o;   // [n_partials][head_dim] unnormalised partial outputs
   float* part_ml;  // [n_partials][2] running max (base 2) and sum
+  // Verify step: accept units appended to the merge grid (acc.n_verify of them).
+  AcceptArgs acc;
 };
 
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
 bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles);
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream);
+// log-sum-exp merge (+ accept of a.acc.n_verify verify threads)
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 
-struct AcceptArgs {
-  const void* logits;
-  int32_t logits_dtype, vocab, n_verify, k_drafts, chunks;
-  const int32_t* drafts;
-  int32_t* accept_len;
-  int32_t* next_token;
-  int32_t* argmax_out;
-  uint64_t* keys;  // [rows][chunks] workspace
-};
+
 int32_t accept_chunks(int32_t rows, int32_t vocab);
 hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream);
 hipError_t launch_accept_tail(const AcceptArgs& a, hipStream_t stream);

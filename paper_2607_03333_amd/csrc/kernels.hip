@@ -30,6 +30,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
+constexpr int kMergeFast = 6;  // outputs with at most this many partials merge with all loads in flight
 constexpr float kLn2 = 0.693147180559945309f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -98,6 +99,130 @@ __device__ __forceinline__ int wave_min_int(int x) {
   for (int o = 32; o >= 1; o >>= 1) x = min(x, __shfl_xor(x, o));
   return x;
 }
+
+// --------------------------------------------------------------------------
+// Greedy argmax, first pass: the best (value, index) of one chunk of a row.
+// Each thread scans its elements in increasing index order keeping the first
+// strict maximum; chunks and threads combine through the 64-bit key
+// (order-preserving value bits << 32) | (0xFFFFFFFF - index), whose maximum
+// is the largest value at the lowest index. -0 is keyed as +0.
+// --------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t argmax_key(float v, int idx) {
+  if (idx == INT_MAX) return 0;
+  uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(idx));
+}
+
+__device__ __forceinline__ float load_f(const float* p, int i) { return p[i]; }
+__device__ __forceinline__ float load_f(const uint16_t* p, int i) {
+  return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
+}
+
+// One (row, chunk) argmax unit run by a workgroup of NT threads; writes the
+// chunk's key to keys[row * chunks + chunk].
+template <typename T, int NT>
+__device__ __forceinline__ void argmax_unit(const AcceptArgs& a, int unit) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int NW = NT / 64;
+  const int row = unit / a.chunks, c = unit % a.chunks;
+  const T* x = static_cast<const T*>(a.logits) + static_cast<size_t>(row) * a.vocab;
+  float best = kNegInf;
+  int bidx = INT_MAX;
+  const bool vec_ok = (a.vocab % VEC) == 0 && (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0;
+  if (vec_ok) {
+    const int nv = a.vocab / VEC;
+    const int lo = static_cast<int>(static_cast<int64_t>(nv) * c / a.chunks);
+    const int hi = static_cast<int>(static_cast<int64_t>(nv) * (c + 1) / a.chunks);
+    const uint4* xv = reinterpret_cast<const uint4*>(x);
+    auto scan = [&](const uint4& u, int v) __attribute__((always_inline)) {
+      const T* e = reinterpret_cast<const T*>(&u);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const float val = load_f(e, j);
+        if (val > best || bidx == INT_MAX) {
+          best = val;
+          bidx = v * VEC + j;
+        }
+      }
+    };
+    // four 16-byte loads in flight per thread, scanned in index order
+    int v = lo + static_cast<int>(threadIdx.x);
+    for (; v + 3 * NT < hi; v += 4 * NT) {
+      const uint4 u0 = xv[v], u1 = xv[v + NT], u2 = xv[v + 2 * NT], u3 = xv[v + 3 * NT];
+      scan(u0, v);
+      scan(u1, v + NT);
+      scan(u2, v + 2 * NT);
+      scan(u3, v + 3 * NT);
+    }
+    for (; v < hi; v += NT) scan(xv[v], v);
+  } else {
+    const int lo = static_cast<int>(static_cast<int64_t>(a.vocab) * c / a.chunks);
+    const int hi = static_cast<int>(static_cast<int64_t>(a.vocab) * (c + 1) / a.chunks);
+    for (int i = lo + static_cast<int>(threadIdx.x); i < hi; i += NT) {
+      const float val = load_f(x, i);
+      if (val > best || bidx == INT_MAX) {
+        best = val;
+        bidx = i;
+      }
+    }
+  }
+  uint64_t key = argmax_key(best, bidx);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint64_t other = __shfl_xor(key, o);
+    key = other > key ? other : key;
+  }
+  if constexpr (NW > 1) {
+    __shared__ uint64_t wk[NW];
+    if ((threadIdx.x & 63) == 0) wk[threadIdx.x >> 6] = key;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t k = wk[0];
+      for (int i = 1; i < NW; ++i) k = wk[i] > k ? wk[i] : k;
+      a.keys[static_cast<size_t>(row) * a.chunks + c] = k;
+    }
+  } else {
+    if (threadIdx.x == 0) a.keys[static_cast<size_t>(row) * a.chunks + c] = key;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) argmax_chunks(AcceptArgs a) {
+  argmax_unit<T, 256>(a, blockIdx.x);
+}
+
+// Accept for verify thread s, run by one wave: combine the chunk keys of its
+// K+1 rows (lane r handles rows r, r+64, ...), then the first draft that
+// differs from the greedy token ends the accepted prefix (a ballot per 64 rows).
+__device__ __forceinline__ int greedy_of(const AcceptArgs& a, int row) {
+  const uint64_t* kp = a.keys + static_cast<size_t>(row) * a.chunks;
+  uint64_t best = 0;
+  for (int c = 0; c < a.chunks; ++c) best = kp[c] > best ? kp[c] : best;
+  return static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(best));
+}
+
+__device__ __forceinline__ void accept_unit(const AcceptArgs& a, int s) {
+  const int lane = threadIdx.x & 63, kd = a.k_drafts;
+  int first = kd;
+  for (int base = 0; base <= kd; base += 64) {
+    const int r = base + lane;
+    bool miss = false;
+    if (r <= kd) {
+      const int g = greedy_of(a, s * (kd + 1) + r);
+      if (a.argmax_out != nullptr) a.argmax_out[s * (kd + 1) + r] = g;
+      miss = r < kd && g != a.drafts[static_cast<size_t>(s) * kd + r];
+    }
+    const uint64_t bal = __ballot(miss);
+    if (bal != 0 && first == kd) first = base + __builtin_ctzll(bal);
+  }
+  if (lane == 0) {
+    a.accept_len[s] = first;
+    a.next_token[s] = greedy_of(a, s * (kd + 1) + first);
+  }
+}
+
+__global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) { accept_unit(a, blockIdx.x); }
 
 // --------------------------------------------------------------------------
 // bf16 partial attention. One workgroup of 4 waves owns a token range of one
@@ -630,29 +755,70 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 template <int D, typename OutT>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int PER = D / 64;
+  const int merge_blocks = (a.n_out + 3) / 4;
+  if (static_cast<int>(blockIdx.x) >= merge_blocks) {
+    // fused accept: one verify thread per wave
+    const int sv = (blockIdx.x - merge_blocks) * 4 + (threadIdx.x >> 6);
+    if (sv < a.acc.n_verify) accept_unit(a.acc, sv);
+    return;
+  }
   const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (o >= a.n_out) return;
   const int beg = a.merge_off[o], end = a.merge_off[o + 1];
-  float mx = kNegInf;
-  for (int c = beg + lane; c < end; c += 64) mx = fmaxf(mx, a.part_ml[2 * a.merge_ids[c]]);
-  mx = wave_max(mx);
-  const float mu = mx == kNegInf ? 0.0f : mx;
-  float sum = 0.0f;
-  for (int c = beg + lane; c < end; c += 64) {
-    const int id = a.merge_ids[c];
-    sum += exp2_fast(a.part_ml[2 * id] - mu) * a.part_ml[2 * id + 1];
-  }
-  sum = wave_sum(sum);
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
-  for (int c = beg; c < end; ++c) {
-    const int id = a.merge_ids[c];
-    const float wgt = exp2_fast(a.part_ml[2 * id] - mu);
-    const float* po = a.part_o + static_cast<size_t>(id) * D + lane * PER;
+  float mu, sum;
+  if (end - beg <= kMergeFast) {
+    // all partial loads issued together: (m, l) pairs and outputs
+    float pm[kMergeFast], pl[kMergeFast], po[kMergeFast][PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += wgt * po[e];
+    for (int i = 0; i < kMergeFast; ++i) {
+      if (beg + i < end) {
+        const int id = a.merge_ids[beg + i];
+        pm[i] = a.part_ml[2 * id];
+        pl[i] = a.part_ml[2 * id + 1];
+        const float* src = a.part_o + static_cast<size_t>(id) * D + lane * PER;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) po[i][e] = src[e];
+      } else {
+        pm[i] = kNegInf;
+        pl[i] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) po[i][e] = 0.0f;
+      }
+    }
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kMergeFast; ++i) mx = fmaxf(mx, pm[i]);
+    mu = mx == kNegInf ? 0.0f : mx;
+    sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMergeFast; ++i) {
+      const float wgt = exp2_fast(pm[i] - mu);
+      sum += wgt * pl[i];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += wgt * po[i][e];
+    }
+  } else {
+    float mx = kNegInf;
+    for (int c = beg + lane; c < end; c += 64) mx = fmaxf(mx, a.part_ml[2 * a.merge_ids[c]]);
+    mx = wave_max(mx);
+    mu = mx == kNegInf ? 0.0f : mx;
+    sum = 0.0f;
+    for (int c = beg + lane; c < end; c += 64) {
+      const int id = a.merge_ids[c];
+      sum += exp2_fast(a.part_ml[2 * id] - mu) * a.part_ml[2 * id + 1];
+    }
+    sum = wave_sum(sum);
+    for (int c = beg; c < end; ++c) {
+      const int id = a.merge_ids[c];
+      const float wgt = exp2_fast(a.part_ml[2 * id] - mu);
+      const float* po = a.part_o + static_cast<size_t>(id) * D + lane * PER;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += wgt * po[e];
+    }
   }
   const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
   OutT* out = static_cast<OutT*>(a.out) + static_cast<size_t>(o) * D + lane * PER;
@@ -660,107 +826,6 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   for (int e = 0; e < PER; ++e) out[e] = static_cast<OutT>(acc[e] * inv);
   if (lane == 0 && a.lse != nullptr)
     a.lse[o] = sum > 0.0f ? (mu + __log2f(sum)) * kLn2 : kNegInf;
-}
-
-// --------------------------------------------------------------------------
-// Greedy argmax, first pass: the best (value, index) of one chunk of a row.
-// Each thread scans its elements in increasing index order keeping the first
-// strict maximum; chunks and threads combine through the 64-bit key
-// (order-preserving value bits << 32) | (0xFFFFFFFF - index), whose maximum
-// is the largest value at the lowest index. -0 is keyed as +0.
-// --------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t argmax_key(float v, int idx) {
-  if (idx == INT_MAX) return 0;
-  uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(idx));
-}
-
-__device__ __forceinline__ float load_f(const float* p, int i) { return p[i]; }
-__device__ __forceinline__ float load_f(const uint16_t* p, int i) {
-  return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
-}
-
-template <typename T>
-__global__ void __launch_bounds__(256) argmax_chunks(AcceptArgs a) {
-  constexpr int VEC = 16 / sizeof(T);
-  const int row = blockIdx.x / a.chunks, c = blockIdx.x % a.chunks;
-  const T* x = static_cast<const T*>(a.logits) + static_cast<size_t>(row) * a.vocab;
-  float best = kNegInf;
-  int bidx = INT_MAX;
-  const bool vec_ok = (a.vocab % VEC) == 0 && (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0;
-  if (vec_ok) {
-    const int nv = a.vocab / VEC;
-    const int lo = static_cast<int>(static_cast<int64_t>(nv) * c / a.chunks);
-    const int hi = static_cast<int>(static_cast<int64_t>(nv) * (c + 1) / a.chunks);
-    for (int v = lo + static_cast<int>(threadIdx.x); v < hi; v += 256) {
-      const uint4 u = reinterpret_cast<const uint4*>(x)[v];
-      const T* e = reinterpret_cast<const T*>(&u);
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) {
-        const float val = load_f(e, j);
-        if (val > best || bidx == INT_MAX) {
-          best = val;
-          bidx = v * VEC + j;
-        }
-      }
-    }
-  } else {
-    const int lo = static_cast<int>(static_cast<int64_t>(a.vocab) * c / a.chunks);
-    const int hi = static_cast<int>(static_cast<int64_t>(a.vocab) * (c + 1) / a.chunks);
-    for (int i = lo + static_cast<int>(threadIdx.x); i < hi; i += 256) {
-      const float val = load_f(x, i);
-      if (val > best || bidx == INT_MAX) {
-        best = val;
-        bidx = i;
-      }
-    }
-  }
-  uint64_t key = argmax_key(best, bidx);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const uint64_t other = __shfl_xor(key, o);
-    key = other > key ? other : key;
-  }
-  __shared__ uint64_t wk[4];
-  if ((threadIdx.x & 63) == 0) wk[threadIdx.x >> 6] = key;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t k = wk[0];
-    for (int i = 1; i < 4; ++i) k = wk[i] > k ? wk[i] : k;
-    a.keys[static_cast<size_t>(row) * a.chunks + c] = k;
-  }
-}
-
-// Accept: per verify thread, combine the chunk keys of its K+1 rows, then the
-// first draft that differs from the greedy token ends the accepted prefix.
-__global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) {
-  extern __shared__ int greedy[];
-  const int s = blockIdx.x, kd = a.k_drafts;
-  for (int r = threadIdx.x; r <= kd; r += 64) {
-    const uint64_t* kp = a.keys + static_cast<size_t>(s * (kd + 1) + r) * a.chunks;
-    uint64_t best = 0;
-    for (int c = 0; c < a.chunks; ++c) best = kp[c] > best ? kp[c] : best;
-    const int idx = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(best));
-    greedy[r] = idx;
-    if (a.argmax_out != nullptr) a.argmax_out[s * (kd + 1) + r] = idx;
-  }
-  __syncthreads();
-  // first mismatch via a ballot over the draft positions
-  int first = kd;
-  for (int base = 0; base < kd; base += 64) {
-    const int r = base + static_cast<int>(threadIdx.x);
-    const bool miss = r < kd && greedy[r] != a.drafts[static_cast<size_t>(s) * kd + r];
-    const uint64_t bal = __ballot(miss);
-    if (bal != 0) {
-      first = base + __builtin_ctzll(bal);
-      break;
-    }
-  }
-  if (threadIdx.x == 0) {
-    a.accept_len[s] = first;
-    a.next_token[s] = greedy[first];
-  }
 }
 
 // --------------------------------------------------------------------------
@@ -862,7 +927,7 @@ hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
-  const int blocks = (a.n_out + 3) / 4;
+  const int blocks = (a.n_out + 3) / 4 + (a.acc.n_verify + 3) / 4;
   if (blocks == 0) return hipSuccess;
   if (a.dtype == 1 && a.head_dim == 128)
     hipLaunchKernelGGL((merge_kernel<128, __bf16>), dim3(blocks), dim3(256), 0, stream, a);
