@@ -172,7 +172,7 @@ def main():
     dw = runner.DeviceWorkload(wl, poison_pool=False)
     steps = dw.prepare_all()
     torch.cuda.synchronize()
-    print(f"# device setup {time.perf_counter() - t_setup:.1f} s; waves {[s.info['n_waves'] for s in steps]} "
+    print(f"# device setup {time.perf_counter() - t_setup:.1f} s; units {[s.info['n_units'] for s in steps]} grid {[s.info['attn_grid'] for s in steps]} "
           f"row tiles {[s.info['max_row_tiles'] for s in steps]}", file=sys.stderr, flush=True)
 
     for _ in range(args.warmup):

@@ -157,10 +157,10 @@ typedef struct spork_plan_info {
   int32_t n_rows;          /* query rows (sum of n_rows) */
   int32_t n_groups;        /* fork groups (cascade units) */
   int32_t n_items;         /* (prefix or suffix range, KV head) work items */
-  int32_t n_waves;         /* attention workgroups launched (incl. padding) */
+  int32_t n_units;         /* attention work units (token range x row slice, incl. padding) */
   int32_t n_partials;      /* partial-result rows written by the attention kernel */
   int32_t max_row_tiles;   /* 16-row MFMA tiles per workgroup */
-  int32_t pad_;
+  int32_t attn_grid;       /* attention workgroups launched */
   size_t image_bytes;      /* size of the device image (spork_plan_image) */
   size_t workspace_bytes;  /* workspace spork_attn_decode needs */
   int64_t shared_tokens;   /* prefix tokens read once per group (sum over groups) */
@@ -193,8 +193,11 @@ int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap);
 /* Batched decode attention of main and probe rows (Sections 4.1 and 4.3).
  * q (device [rows][Hq][D] dtype); k_cache, v_cache (device pools);
  * out (device [rows][Hq][D] dtype); lse (device [rows][Hq] float32, nullable);
- * workspace (device, ws_bytes >= info.workspace_bytes, any contents).
- * Kernels: cascade partial attention over prefix and suffix ranges, then the
+ * workspace (device, ws_bytes >= info.workspace_bytes, any contents on
+ * entry; it holds the partial results and the attention's list cursors, so
+ * calls that share a workspace must not overlap).
+ * Kernels, in order on `stream`: a small kernel that zeroes the list cursors
+ * (bf16), the cascade partial attention over prefix and suffix ranges, the
  * log-sum-exp merge. */
 int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void* q,
                       const void* k_cache, const void* v_cache, void* out, float* lse,
@@ -216,8 +219,9 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
  * Ties pick the lowest vocabulary index; logits must be finite.
  * workspace: the attention's workspace followed (at a 256-byte aligned
  * offset) by spork_verify_workspace_bytes; ws_bytes covers both.
- * With a plan the step is three launches on `stream`: partial attention,
- * argmax, then the merge together with the accept. */
+ * With a plan the step is three launches on `stream`: argmax (which also
+ * zeroes the attention's list cursors), partial attention, then the merge
+ * together with the accept. */
 int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q,
                         const void* k_cache, const void* v_cache, void* out, float* lse,
                         const void* logits, int32_t logits_dtype, int32_t vocab,

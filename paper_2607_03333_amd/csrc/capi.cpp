@@ -59,10 +59,12 @@ hipError_t timed(int kind, hipStream_t stream, F&& f) {
   const size_t at = g_timing.used;
   hipEvent_t b = next_event(), e = next_event();
   if (b == nullptr || e == nullptr) return hipErrorOutOfMemory;
-  hipEventRecord(b, stream);
-  const hipError_t rc = f();
-  hipEventRecord(e, stream);
-  g_timing.marks.push_back({kind, at});
+  hipError_t rc = hipEventRecord(b, stream);
+  if (rc != hipSuccess) return rc;
+  rc = f();
+  if (rc != hipSuccess) return rc;
+  rc = hipEventRecord(e, stream);
+  if (rc == hipSuccess) g_timing.marks.push_back({kind, at});
   return rc;
 }
 
@@ -260,12 +262,12 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
       return fail(SPORK_E_INVAL, "NULL argument");
     int rc = check_shape(shape);
     if (rc != SPORK_OK) return rc;
-    // bf16: 4-wave workgroups with up to 2 row tiles per wave, 2 per CU
-    // (their 68 KB of LDS); fp32: 1-wave workgroups with up to 4 row tiles,
-    // 4 per CU (8 with up to 2 tiles).
+    // bf16: persistent 4-wave workgroups with up to 2 row tiles per wave,
+    // 2 per CU (their 68 KB of LDS); fp32: one 1-wave workgroup per unit with
+    // up to 4 row tiles, 4 per CU (8 with up to 2 tiles).
     const bool bf16 = shape->dtype == SPORK_DTYPE_BF16;
     spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype),
-                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 2 : 8};
+                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 2 : 8, bf16};
     auto* plan = new spork_plan();
     plan->shape = *shape;
     const std::string err = spork::build_plan(cache->bm, ps, seqs, n_rows, groups, n_threads, n_cu, &plan->p);
@@ -291,7 +293,8 @@ int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info) {
   info->n_rows = p.n_rows;
   info->n_groups = p.n_groups;
   info->n_items = p.n_items;
-  info->n_waves = p.n_waves;
+  info->n_units = p.n_units;
+  info->attn_grid = p.grid;
   info->n_partials = p.n_partials;
   info->max_row_tiles = p.row_tiles;
   info->image_bytes = p.image.size();
@@ -311,8 +314,8 @@ int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap) {
   return SPORK_OK;
 }
 
-// Attention over a plan; with `acc` (a verify step) the argmax runs after the
-// attention and the accept rides in the merge launch.
+// Attention over a plan; with `acc` (a verify step) the argmax runs first and
+// the accept rides in the merge launch.
 static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
                      const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
                      const spork::AcceptArgs* acc, hipStream_t stream) {
@@ -336,7 +339,11 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.tables = reinterpret_cast<const int32_t*>(img + p.off_tables);
   a.merge_off = reinterpret_cast<const int32_t*>(img + p.off_merge_off);
   a.merge_ids = reinterpret_cast<const int32_t*>(img + p.off_merge_ids);
-  a.n_waves = p.n_waves;
+  a.wg_off = reinterpret_cast<const int32_t*>(img + p.off_wg_off);
+  a.cursors = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + p.off_ws_cursors);
+  a.n_units = p.n_units;
+  a.grid = p.grid;
+  a.n_lists = p.n_lists;
   a.n_out = p.n_out;
   a.row_tiles = p.row_tiles;
   a.hq = sh.hq;
@@ -352,16 +359,25 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.lse = lse;
   a.part_o = static_cast<float*>(workspace);
   a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
+  // The persistent bf16 kernel needs its list cursors at zero: a verify step
+  // runs the argmax first, which clears them (the accept then rides in the
+  // merge launch); a decode step clears them with a small kernel.
+  const bool persistent = p.shape.persistent;
   const bool verify = acc != nullptr && acc->n_verify > 0;
-  if (verify) a.acc = *acc;
-  int rc = hip_status(timed(SPORK_KERNEL_ATTN, stream, [&] { return spork::launch_attn_partial(a, stream); }),
-                      "spork_attn_decode (partial attention)");
-  if (rc != SPORK_OK) return rc;
+  int rc = SPORK_OK;
   if (verify) {
-    rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(*acc, stream); }),
+    a.acc = *acc;
+    a.acc.counters = persistent ? a.cursors : nullptr;
+    a.acc.n_counters = persistent ? p.n_lists : 0;
+    rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(a.acc, stream); }),
                     "spork_verify_accept (argmax)");
-    if (rc != SPORK_OK) return rc;
+  } else if (persistent) {
+    rc = hip_status(spork::launch_counter_reset(a.cursors, p.n_lists, stream), "spork_attn_decode (cursor reset)");
   }
+  if (rc != SPORK_OK) return rc;
+  rc = hip_status(timed(SPORK_KERNEL_ATTN, stream, [&] { return spork::launch_attn_partial(a, stream); }),
+                  "spork_attn_decode (partial attention)");
+  if (rc != SPORK_OK) return rc;
   return hip_status(timed(SPORK_KERNEL_MERGE, stream, [&] { return spork::launch_merge(a, stream); }),
                     "spork_attn_decode (merge)");
 }

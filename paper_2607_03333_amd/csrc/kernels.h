@@ -18,6 +18,10 @@ struct AcceptArgs {
   int32_t* next_token;
   int32_t* argmax_out;
   uint64_t* keys;  // [rows][chunks] workspace
+  // nullable: int32 counters of the attention launch that follows, which the
+  // argmax launch clears
+  int32_t* counters;
+  int32_t n_counters;
 };
 
 struct AttnArgs {
@@ -27,7 +31,11 @@ struct AttnArgs {
   const int32_t* tables;
   const int32_t* merge_off;
   const int32_t* merge_ids;
-  int32_t n_waves, n_out, row_tiles;
+  // Unit lists (CSR over waves): the bf16 kernel's workgroup b takes the units
+  // of list b % n_lists in order, through cursors[list] (zero before the launch).
+  const int32_t* wg_off;
+  int32_t* cursors;
+  int32_t n_units, grid, n_lists, n_out, row_tiles;
   int32_t hq, hkv, head_dim, block_size, dtype;
   float scale_log2;  // sm_scale * log2(e): scores are kept in base 2
   const void* q;
@@ -44,6 +52,8 @@ struct AttnArgs {
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
 bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles);
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream);
+// zero n int32 counters (the list cursors, before a persistent attention launch)
+hipError_t launch_counter_reset(int32_t* counters, int32_t n, hipStream_t stream);
 // log-sum-exp merge (+ accept of a.acc.n_verify verify threads)
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 

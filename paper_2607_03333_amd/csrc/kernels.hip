@@ -30,7 +30,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
-constexpr int kMergeFast = 6;  // outputs with at most this many partials merge with all loads in flight
 constexpr float kLn2 = 0.693147180559945309f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -189,6 +188,8 @@ __device__ __forceinline__ void argmax_unit(const AcceptArgs& a, int unit) {
 
 template <typename T>
 __global__ void __launch_bounds__(256) argmax_chunks(AcceptArgs a) {
+  if (a.counters != nullptr)
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < a.n_counters; i += gridDim.x * 256) a.counters[i] = 0;
   argmax_unit<T, 256>(a, blockIdx.x);
 }
 
@@ -225,9 +226,9 @@ __device__ __forceinline__ void accept_unit(const AcceptArgs& a, int s) {
 __global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) { accept_unit(a, blockIdx.x); }
 
 // --------------------------------------------------------------------------
-// bf16 partial attention. One workgroup of 4 waves owns a token range of one
-// work item and up to 4*RTW 16-row tiles of its query rows; wave w computes
-// tiles w, w+4, ... . The range streams through a ring of kRing LDS slots, one
+// bf16 partial attention. A persistent workgroup of 4 waves works through its
+// list of units; a unit is a token range of one work item and up to 4*RTW
+// 16-row tiles of its query rows; wave w computes tiles w, w+4, ... . The range streams through a ring of kRing LDS slots, one
 // 32-token K/V tile ("stage", 16 KB) each, filled by direct global-to-LDS
 // 16-byte loads (global_load_lds_dwordx4: lane i of an instruction lands at
 // the instruction's LDS base + 16*i), so kRing-1 stages stay in flight without
@@ -331,10 +332,20 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   static_assert(BS == 16 || BS == 32, "unsupported block size");
   __shared__ uint4 smem[kRing][kStageChunks];
   __shared__ int tab[kUnitBlocks];
-  const WaveDesc w = a.waves[blockIdx.x];
-  if (w.item < 0) return;
-  const ItemDesc it = a.items[w.item];
+  __shared__ int next_unit;
+  // Persistent workgroup: it takes the next unit of its compute unit's list
+  // (shared with the other workgroup resident there) until the list is done.
   const int tid = threadIdx.x;
+  const int list = static_cast<int>(blockIdx.x) % a.n_lists;
+  const int list0 = a.wg_off[list], list_len = a.wg_off[list + 1] - list0;
+  for (;;) {
+  if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
+  __syncthreads();
+  const int taken = __builtin_amdgcn_readfirstlane(next_unit);
+  if (taken >= list_len) break;
+  const WaveDesc w = a.waves[list0 + taken];
+  if (w.item < 0) continue;
+  const ItemDesc it = a.items[w.item];
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ qg = static_cast<const uint16_t*>(a.q);
@@ -595,6 +606,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   if (RTW >= 2 && nown == 2) run(std::integral_constant<int, (RTW >= 2 ? 2 : 1)>{});
   else if (nown == 1) run(std::integral_constant<int, 1>{});
   else run(std::integral_constant<int, 0>{});
+  // The next take's barrier is reached by every wave only after its last
+  // reads of this unit's ring slots, table and next_unit.
+  }
 }
 
 // --------------------------------------------------------------------------
@@ -751,7 +765,56 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 //   M = max m_i, L = sum 2^(m_i - M) l_i, O = sum 2^(m_i - M) o_i / L,
 //   lse = (M + log2 L) ln 2. Partials with nothing visible (m = -inf, l = 0)
 //   add nothing.
+// Partials go in batches of 4 (outputs with at most 4) or 8: the batch's
+// partial ids come with one vector load (lane i: entry i), then the (m, l)
+// pairs and all output rows are loaded together, so a batch costs two memory
+// round trips whatever its size; unused slots repeat a valid id with weight
+// 0. Batches after the first rescale the running sums to the new maximum.
 // --------------------------------------------------------------------------
+// One batch of at most B partials (entries c0 .. c0 + k - 1 of the output's
+// list), folded into the running (max, sum, accumulator).
+template <int B, int D>
+__device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bool first, int lane, float& run_max,
+                                            float& mu, float& sum, float (&acc)[D / 64]) {
+  constexpr int PER = D / 64;
+  const int id = a.merge_ids[c0 + min(lane, k - 1)];
+  const float2 ml = reinterpret_cast<const float2*>(a.part_ml)[id];
+  float po[B][PER];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const int idi = __builtin_amdgcn_readlane(id, i);
+    const float* src = a.part_o + static_cast<size_t>(idi) * D + lane * PER;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) po[i][e] = src[e];
+  }
+  const bool live = lane < k;
+  const float pm = live ? ml.x : kNegInf;
+  const float pl = live ? ml.y : 0.0f;
+  float bm = kNegInf;
+#pragma unroll
+  for (int i = 0; i < B; ++i)
+    bm = fmaxf(bm, __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pm), i)));
+  const float new_max = fmaxf(run_max, bm);
+  const float new_mu = new_max == kNegInf ? 0.0f : new_max;
+  if (!first) {
+    const float alpha = exp2_fast(mu - new_mu);
+    sum *= alpha;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] *= alpha;
+  }
+  run_max = new_max;
+  mu = new_mu;
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const float mi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pm), i));
+    const float li = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pl), i));
+    const float wgt = exp2_fast(mi - mu);  // 0 for unused slots (mi = -inf)
+    sum += wgt * li;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += wgt * po[i][e];
+  }
+}
+
 template <int D, typename OutT>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int PER = D / 64;
@@ -769,56 +832,11 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
-  float mu, sum;
-  if (end - beg <= kMergeFast) {
-    // all partial loads issued together: (m, l) pairs and outputs
-    float pm[kMergeFast], pl[kMergeFast], po[kMergeFast][PER];
-#pragma unroll
-    for (int i = 0; i < kMergeFast; ++i) {
-      if (beg + i < end) {
-        const int id = a.merge_ids[beg + i];
-        pm[i] = a.part_ml[2 * id];
-        pl[i] = a.part_ml[2 * id + 1];
-        const float* src = a.part_o + static_cast<size_t>(id) * D + lane * PER;
-#pragma unroll
-        for (int e = 0; e < PER; ++e) po[i][e] = src[e];
-      } else {
-        pm[i] = kNegInf;
-        pl[i] = 0.0f;
-#pragma unroll
-        for (int e = 0; e < PER; ++e) po[i][e] = 0.0f;
-      }
-    }
-    float mx = kNegInf;
-#pragma unroll
-    for (int i = 0; i < kMergeFast; ++i) mx = fmaxf(mx, pm[i]);
-    mu = mx == kNegInf ? 0.0f : mx;
-    sum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kMergeFast; ++i) {
-      const float wgt = exp2_fast(pm[i] - mu);
-      sum += wgt * pl[i];
-#pragma unroll
-      for (int e = 0; e < PER; ++e) acc[e] += wgt * po[i][e];
-    }
+  float mu = 0.0f, sum = 0.0f, run_max = kNegInf;
+  if (end - beg <= 4) {
+    merge_batch<4, D>(a, beg, end - beg, true, lane, run_max, mu, sum, acc);
   } else {
-    float mx = kNegInf;
-    for (int c = beg + lane; c < end; c += 64) mx = fmaxf(mx, a.part_ml[2 * a.merge_ids[c]]);
-    mx = wave_max(mx);
-    mu = mx == kNegInf ? 0.0f : mx;
-    sum = 0.0f;
-    for (int c = beg + lane; c < end; c += 64) {
-      const int id = a.merge_ids[c];
-      sum += exp2_fast(a.part_ml[2 * id] - mu) * a.part_ml[2 * id + 1];
-    }
-    sum = wave_sum(sum);
-    for (int c = beg; c < end; ++c) {
-      const int id = a.merge_ids[c];
-      const float wgt = exp2_fast(a.part_ml[2 * id] - mu);
-      const float* po = a.part_o + static_cast<size_t>(id) * D + lane * PER;
-#pragma unroll
-      for (int e = 0; e < PER; ++e) acc[e] += wgt * po[e];
-    }
+    for (int c0 = beg; c0 < end; c0 += 8) merge_batch<8, D>(a, c0, min(8, end - c0), c0 == beg, lane, run_max, mu, sum, acc);
   }
   const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
   OutT* out = static_cast<OutT*>(a.out) + static_cast<size_t>(o) * D + lane * PER;
@@ -873,6 +891,10 @@ __global__ void __launch_bounds__(256) kv_copy_kernel(int hkv, int D, int BS, T*
   vc[vd] = vc[vs];
 }
 
+__global__ void __launch_bounds__(256) counter_reset_kernel(int32_t* counters, int32_t n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) counters[i] = 0;
+}
+
 // --------------------------------------------------------------------------
 // Dispatch tables.
 // --------------------------------------------------------------------------
@@ -922,7 +944,14 @@ hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream) {
   AttnKernel k = pick_attention(a.dtype, a.head_dim, a.block_size, a.row_tiles);
   if (k == nullptr) return hipErrorInvalidValue;
   const int threads = a.dtype == 1 ? 64 * kWgWaves : 64;
-  if (a.n_waves > 0) hipLaunchKernelGGL(k, dim3(a.n_waves), dim3(threads), 0, stream, a);
+  if (a.grid > 0) hipLaunchKernelGGL(k, dim3(a.grid), dim3(threads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_counter_reset(int32_t* counters, int32_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = n / 256 + 1 < 64 ? n / 256 + 1 : 64;
+  hipLaunchKernelGGL(counter_reset_kernel, dim3(blocks), dim3(256), 0, stream, counters, n);
   return hipGetLastError();
 }
 

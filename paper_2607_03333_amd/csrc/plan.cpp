@@ -23,6 +23,15 @@ struct Unit {  // one token segment of one item, split over `slices` row slices
   int64_t cost() const { return static_cast<int64_t>(hi - lo) * slices; }
 };
 
+// End of a unit cut from [lo, rest_hi) that asks for about `want` tokens
+// (at least min_piece, at most kMaxUnitTokens): on a tile boundary, or the
+// end of the range.
+int32_t cut_piece(int32_t lo, int32_t rest_hi, int64_t want, int64_t min_piece) {
+  want = std::min<int64_t>(std::max<int64_t>(want, min_piece), kMaxUnitTokens);
+  const int64_t hi = (static_cast<int64_t>(lo) + want + kTileTokens - 1) / kTileTokens * kTileTokens;
+  return hi >= rest_hi ? rest_hi : static_cast<int32_t>(hi);
+}
+
 }  // namespace
 
 std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int32_t* seqs,
@@ -153,84 +162,195 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   }
   p.n_items = static_cast<int32_t>(items.size());
 
-  // Split-K: cut every item into token segments of near-equal cost so that
-  // about one full-occupancy round of workgroups covers the batch.
+  // Split-K. Items are cut into work units (token range x row slice).
   const int32_t per_cu = 2 * row_tiles <= shape.unit_tiles_max ? shape.units_per_cu_half : shape.units_per_cu;
-  const int64_t target = static_cast<int64_t>(n_cu) * std::max(1, per_cu);
-  int64_t cost = 0;
-  for (size_t it = 0; it < items.size(); ++it) {
-    const Range& rg = *item_range[it];
-    const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
-    cost += static_cast<int64_t>(rg.hi - rg.lo) * slices;
-  }
-  // Ideal tokens per workgroup slot; each item is cut into round(len / ideal)
-  // pieces (at least 1, at most kMaxUnitTokens long) so that equal items fill
-  // whole rounds of the resident workgroups.
-  const double ideal = std::max(1.0, static_cast<double>(cost) / static_cast<double>(target));
-
-  std::vector<Unit> units;
-  for (size_t it = 0; it < items.size(); ++it) {
-    const Range& rg = *item_range[it];
-    const int32_t slices = (items[it].n_rows + slice_rows - 1) / slice_rows;
-    const int64_t n = rg.hi - rg.lo;
-    int64_t nseg = std::max<int64_t>(1, static_cast<int64_t>(static_cast<double>(n) / ideal + 0.5));
-    nseg = std::max<int64_t>(nseg, (n + kMaxUnitTokens - 1) / kMaxUnitTokens);
-    nseg = std::min<int64_t>(nseg, std::max<int64_t>(1, n / kTileTokens));
-    int32_t lo = rg.lo;
-    for (int64_t k = 1; k <= nseg; ++k) {
-      int32_t hi = rg.hi;
-      if (k < nseg) {
-        const int64_t cut = rg.lo + n * k / nseg;
-        hi = static_cast<int32_t>((cut + kTileTokens / 2) / kTileTokens * kTileTokens);
-        if (hi <= lo || hi >= rg.hi) continue;
-      }
-      // block-table span the kernel stages for this unit (kernel tables hold 1040)
-      const int32_t tb0 = lo / kTileTokens * kTileTokens;
-      const int32_t span_end = tb0 + (hi - tb0 + kTileTokens - 1) / kTileTokens * kTileTokens + 16;
-      if (span_end / shape.block_size - tb0 / shape.block_size + 1 > 1040) return "internal: unit too long";
-      units.push_back({static_cast<int32_t>(it), lo, hi, slices});
-      lo = hi;
-    }
-  }
-
-  // Longest first, each unit to the least-loaded die; a unit's row slices are
-  // adjacent in its die's queue so they run together and share that die's L2.
-  std::stable_sort(units.begin(), units.end(),
-                   [](const Unit& a, const Unit& b) { return a.hi - a.lo > b.hi - b.lo; });
-  std::vector<std::vector<WaveDesc>> queue(kXcds);
-  std::vector<int64_t> load(kXcds, 0);
-  for (const Unit& u : units) {
-    const int x = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
-    load[x] += u.cost();
-    const int32_t nr = items[u.item].n_rows;
-    for (int32_t s = 0; s < u.slices; ++s) {
-      WaveDesc w{};
-      w.item = u.item;
-      w.tok_lo = u.lo;
-      w.tok_hi = u.hi;
-      w.row0 = s * slice_rows;
-      w.nrows = std::min(slice_rows, nr - s * slice_rows);
-      queue[x].push_back(w);
-    }
-  }
-  size_t depth = 0;
-  for (const auto& q : queue) depth = std::max(depth, q.size());
+  const int64_t n_wg = static_cast<int64_t>(n_cu) * std::max(1, per_cu);
+  std::vector<int32_t> slices_of(items.size());
+  for (size_t it = 0; it < items.size(); ++it) slices_of[it] = (items[it].n_rows + slice_rows - 1) / slice_rows;
   std::vector<WaveDesc> waves;
-  waves.reserve(depth * kXcds);
-  int32_t partial = 0;
-  for (size_t d = 0; d < depth; ++d) {
-    for (int x = 0; x < kXcds; ++x) {
-      if (d < queue[x].size()) {
-        WaveDesc w = queue[x][d];
-        w.partial = partial;
-        partial += w.nrows;
-        waves.push_back(w);
-      } else {
-        waves.push_back({-1, 0, 0, 0, 0, 0});
+  std::vector<int32_t> wg_off;
+  auto desc = [&](int32_t item, int32_t lo, int32_t hi, int32_t s) {
+    WaveDesc w{};
+    w.item = item;
+    w.tok_lo = lo;
+    w.tok_hi = hi;
+    w.row0 = s * slice_rows;
+    w.nrows = std::min(slice_rows, items[item].n_rows - s * slice_rows);
+    return w;
+  };
+  if (shape.persistent) {
+    // Persistent launch: n_wg resident workgroups. Units go on one list per
+    // compute unit, shared by the workgroups resident on it (workgroups c and
+    // c + n_wg/2 when two share a compute unit), which take the list's units
+    // in order through an atomic cursor: the faster workgroup of the pair
+    // (the one dispatched first wins the instruction arbiter by age) simply
+    // takes more units, and compute units differ little in throughput, so a
+    // static balance between the lists suffices. A range with two row slices
+    // puts both slices next to each other on one list, so the pair streams
+    // its KV through one L2 at the same time.
+    //
+    // Lists are balanced by water-filling on token cost, each unit also
+    // costing kUnitOverheadTokens for its start-up: ranges shorter than half
+    // a list's share go whole, longest first, to the least-loaded list;
+    // longer ranges are cut so that each piece tops the least-loaded list up
+    // to the share, a piece being at most one workgroup's share so that both
+    // workgroups of a list find work. Each list runs longest unit first, so
+    // its last units are short.
+    const int64_t per_list = per_cu == 2 ? 2 : 1;
+    const int64_t lanes = n_wg / per_list;
+    std::vector<std::vector<WaveDesc>> lists(lanes);
+    std::vector<int64_t> load(lanes, 0);
+    auto least = [&]() {
+      return static_cast<int64_t>(std::min_element(load.begin(), load.end()) - load.begin());
+    };
+    auto place = [&](int32_t item, int32_t lo, int32_t hi, int32_t slices) {
+      const int64_t c = least();
+      for (int32_t s = 0; s < slices; ++s) lists[c].push_back(desc(item, lo, hi, s));
+      load[c] += (static_cast<int64_t>(hi - lo) + kUnitOverheadTokens) * slices;
+    };
+    std::vector<size_t> order(items.size());
+    for (size_t i = 0; i < order.size(); ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](size_t x, size_t y) {
+      return item_range[x]->hi - item_range[x]->lo > item_range[y]->hi - item_range[y]->lo;
+    });
+    // The share of a list: the fixed point of share = (tokens +
+    // kUnitOverheadTokens * units) / lanes, where a range shorter than half
+    // the share is one unit per slice and a longer one is cut into pieces of
+    // share / max(slices, workgroups per list) - kUnitOverheadTokens.
+    int64_t tokens = 0;
+    for (size_t it = 0; it < items.size(); ++it)
+      tokens += static_cast<int64_t>(item_range[it]->hi - item_range[it]->lo) * slices_of[it];
+    auto unit_cost_share = [&](int64_t share) {
+      int64_t units = 0;
+      for (size_t it = 0; it < items.size(); ++it) {
+        const int64_t len = item_range[it]->hi - item_range[it]->lo;
+        const int64_t piece =
+            std::max<int64_t>(kTileTokens, share / std::max<int64_t>(slices_of[it], per_list) - kUnitOverheadTokens);
+        units += ((len + kUnitOverheadTokens) * slices_of[it] <= share / 2 ? 1 : (len + piece - 1) / piece) *
+                 slices_of[it];
+      }
+      return (tokens + kUnitOverheadTokens * units + lanes - 1) / lanes;
+    };
+    int64_t share = (tokens + lanes - 1) / lanes;
+    for (int iter = 0; iter < 32; ++iter) {
+      const int64_t next = unit_cost_share(share);
+      if (next == share) break;
+      share = (share + next + 1) / 2;
+    }
+    // Fill towards `level`; what is left once every list has reached it (the
+    // estimate's unit count was short) goes out in short pieces, each with
+    // its own start-up cost; the level is then raised by that overflow spread
+    // over all lists and the fill repeated, keeping the lowest maximum.
+    const int64_t min_piece =  // an eighth of a workgroup's share, 64..512 tokens
+        std::min<int64_t>(kMinPieceTokens, std::max<int64_t>(64, share / per_list / 8 / kTileTokens * kTileTokens));
+    auto fill = [&](int64_t level, int64_t* overflow) {
+      for (auto& l : lists) l.clear();
+      std::fill(load.begin(), load.end(), 0);
+      *overflow = 0;
+      for (int pass = 0; pass < 2; ++pass) {
+        for (size_t it : order) {
+          const Range& rg = *item_range[it];
+          const int32_t slices = slices_of[it];
+          const bool small = (static_cast<int64_t>(rg.hi - rg.lo) + kUnitOverheadTokens) * slices <= share / 2;
+          if (small != (pass == 0)) continue;
+          for (int32_t lo = rg.lo; lo < rg.hi;) {
+            int64_t want = kMaxUnitTokens;
+            // a piece tops the list up, but is at most one workgroup's share
+            if (!small) want = std::min(level - load[least()], level / per_list * slices) / slices - kUnitOverheadTokens;
+            const int32_t hi = cut_piece(lo, rg.hi, want, min_piece);
+            if (!small && want < min_piece) *overflow += (hi - lo + kUnitOverheadTokens) * slices;
+            place(static_cast<int32_t>(it), lo, hi, slices);
+            lo = hi;
+          }
+        }
+      }
+      return *std::max_element(load.begin(), load.end());
+    };
+    std::vector<std::vector<WaveDesc>> best;
+    int64_t best_max = INT64_MAX, level = share;
+    for (int round = 0; round < 6; ++round) {
+      int64_t overflow = 0;
+      const int64_t mx = fill(level, &overflow);
+      if (mx < best_max) {
+        best_max = mx;
+        best = lists;
+      }
+      if (overflow == 0) break;
+      level += std::max<int64_t>(kTileTokens, (overflow + lanes - 1) / lanes);
+    }
+    lists.swap(best);
+    wg_off.push_back(0);
+    for (auto& l : lists) {
+      // longest unit first; the row slices of a piece stay adjacent
+      std::stable_sort(l.begin(), l.end(), [](const WaveDesc& x, const WaveDesc& y) {
+        const int32_t lx = x.tok_hi - x.tok_lo, ly = y.tok_hi - y.tok_lo;
+        if (lx != ly) return lx > ly;
+        if (x.item != y.item) return x.item < y.item;
+        if (x.tok_lo != y.tok_lo) return x.tok_lo < y.tok_lo;
+        return x.row0 < y.row0;
+      });
+      waves.insert(waves.end(), l.begin(), l.end());
+      wg_off.push_back(static_cast<int32_t>(waves.size()));
+    }
+    p.grid = static_cast<int32_t>(n_wg);
+    p.n_lists = static_cast<int32_t>(lanes);
+  } else {
+    // One workgroup per unit: items cut into round(len / ideal) segments of
+    // near-equal cost (ideal: the batch's cost over the resident workgroups),
+    // longest first, each to the least-loaded die; workgroup ids are dealt to
+    // the dies round-robin, so a unit's row slices stay on one die's L2.
+    int64_t cost = 0;
+    for (size_t it = 0; it < items.size(); ++it)
+      cost += static_cast<int64_t>(item_range[it]->hi - item_range[it]->lo) * slices_of[it];
+    const double ideal = std::max(1.0, static_cast<double>(cost) / static_cast<double>(n_wg));
+    std::vector<Unit> units;
+    for (size_t it = 0; it < items.size(); ++it) {
+      const Range& rg = *item_range[it];
+      const int64_t n = rg.hi - rg.lo;
+      int64_t nseg = std::max<int64_t>(1, static_cast<int64_t>(static_cast<double>(n) / ideal + 0.5));
+      nseg = std::max<int64_t>(nseg, (n + kMaxUnitTokens - 1) / kMaxUnitTokens);
+      nseg = std::min<int64_t>(nseg, std::max<int64_t>(1, n / kTileTokens));
+      int32_t lo = rg.lo;
+      for (int64_t k = 1; k <= nseg; ++k) {
+        int32_t hi = rg.hi;
+        if (k < nseg) {
+          const int64_t cut = rg.lo + n * k / nseg;
+          hi = static_cast<int32_t>((cut + kTileTokens / 2) / kTileTokens * kTileTokens);
+          if (hi <= lo || hi >= rg.hi) continue;
+        }
+        units.push_back({static_cast<int32_t>(it), lo, hi, slices_of[it]});
+        lo = hi;
       }
     }
+    std::stable_sort(units.begin(), units.end(),
+                     [](const Unit& a, const Unit& b) { return a.hi - a.lo > b.hi - b.lo; });
+    std::vector<std::vector<WaveDesc>> queue(kXcds);
+    std::vector<int64_t> load(kXcds, 0);
+    for (const Unit& u : units) {
+      const int x = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+      load[x] += u.cost();
+      for (int32_t s = 0; s < u.slices; ++s) queue[x].push_back(desc(u.item, u.lo, u.hi, s));
+    }
+    size_t depth = 0;
+    for (const auto& q : queue) depth = std::max(depth, q.size());
+    for (size_t d = 0; d < depth; ++d)
+      for (int x = 0; x < kXcds; ++x)
+        waves.push_back(d < queue[x].size() ? queue[x][d] : WaveDesc{-1, 0, 0, 0, 0, 0});
+    for (size_t i = 0; i <= waves.size(); ++i) wg_off.push_back(static_cast<int32_t>(i));
+    p.grid = static_cast<int32_t>(waves.size());
+    p.n_lists = p.grid;
   }
-  p.n_waves = static_cast<int32_t>(waves.size());
+  int32_t partial = 0;
+  for (WaveDesc& w : waves) {
+    if (w.item < 0) continue;
+    // block-table span the bf16 kernel stages for this unit (1040 entries)
+    const int32_t tb0 = w.tok_lo / kTileTokens * kTileTokens;
+    const int32_t span_end = tb0 + (w.tok_hi - tb0 + kTileTokens - 1) / kTileTokens * kTileTokens + 16;
+    if (span_end / shape.block_size - tb0 / shape.block_size + 1 > 1040) return "internal: unit too long";
+    w.partial = partial;
+    partial += w.nrows;
+  }
+  p.n_units = static_cast<int32_t>(waves.size());
   p.n_partials = partial;
 
   // Merge lists: the partial rows of every output (query row x query head).
@@ -265,6 +385,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   p.off_tables = place(tables.size() * sizeof(int32_t));
   p.off_merge_off = place(count.size() * sizeof(int32_t));
   p.off_merge_ids = place(merge_ids.size() * sizeof(int32_t));
+  p.off_wg_off = place(wg_off.size() * sizeof(int32_t));
   p.image.assign(off, 0);
   auto put = [&](size_t at, const void* src, size_t bytes) {
     if (bytes) std::memcpy(p.image.data() + at, src, bytes);
@@ -275,10 +396,12 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   put(p.off_tables, tables.data(), tables.size() * sizeof(int32_t));
   put(p.off_merge_off, count.data(), count.size() * sizeof(int32_t));
   put(p.off_merge_ids, merge_ids.data(), merge_ids.size() * sizeof(int32_t));
+  put(p.off_wg_off, wg_off.data(), wg_off.size() * sizeof(int32_t));
 
   const size_t o_bytes = align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
   p.off_ws_ml = o_bytes;
-  p.workspace_bytes = o_bytes + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
+  p.off_ws_cursors = o_bytes + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
+  p.workspace_bytes = p.off_ws_cursors + align256(static_cast<size_t>(p.n_lists) * sizeof(int32_t));
   *out = std::move(p);
   return "";
 }

@@ -4,9 +4,9 @@
 // tables (capped so that every row may see all of it); that prefix is one
 // work item per KV head whose rows are all members' rows, so its KV is read
 // once per group. Each thread's remaining positions form its own item. Items
-// are cut into token ranges of near-equal size (split-K), one workgroup per
-// (range, row slice), and every output row lists the partial results the
-// log-sum-exp merge combines.
+// are cut into work units (token range x row slice, split-K) on lists of
+// near-equal cost, one per compute unit, and every output row lists the
+// partial results the log-sum-exp merge combines.
 #pragma once
 
 #include <cstddef>
@@ -24,19 +24,22 @@ struct PlanShape {
   int32_t unit_tiles_max;  // 16-row tiles one attention workgroup can hold
   int32_t units_per_cu;    // attention workgroups resident per compute unit
   int32_t units_per_cu_half;  // the same when every workgroup needs at most half the tiles
+  bool persistent;         // resident workgroups each work through a list of units
 };
 
 struct Plan {
   PlanShape shape{};
   int32_t n_threads = 0, n_rows = 0, n_groups = 0, n_items = 0;
-  int32_t n_waves = 0, n_partials = 0, row_tiles = 1, n_out = 0;
+  int32_t n_units = 0, grid = 0, n_partials = 0, row_tiles = 1, n_out = 0;
+  int32_t n_lists = 0;  // unit lists (persistent launch: one per compute unit)
   int64_t shared_tokens = 0, private_tokens = 0, flat_tokens = 0;
   // device image: sections at 256-byte aligned byte offsets
   std::vector<uint8_t> image;
   size_t off_waves = 0, off_items = 0, off_rows = 0, off_tables = 0, off_merge_off = 0,
-         off_merge_ids = 0;
-  size_t workspace_bytes = 0;  // partial outputs + (m, l) pairs
+         off_merge_ids = 0, off_wg_off = 0;
+  size_t workspace_bytes = 0;  // partial outputs + (m, l) pairs + list cursors
   size_t off_ws_ml = 0;        // byte offset of the (m, l) pairs in the workspace
+  size_t off_ws_cursors = 0;   // byte offset of the list cursors (zeroed before each launch)
 };
 
 // Returns "" on success, else an error message (nothing is built).

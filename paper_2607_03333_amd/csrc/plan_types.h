@@ -4,9 +4,9 @@
 
 namespace spork {
 
-// One attention workgroup: a token range of one work item and a slice of the
-// item's query rows. item < 0 marks a padding workgroup that exits at once.
-// (The bf16 kernel runs a workgroup as 4 waves, the fp32 kernel as 1.)
+// One attention work unit: a token range of one work item and a slice of the
+// item's query rows. item < 0 marks padding that is skipped. (The bf16 kernel
+// runs units on 4-wave workgroups, the fp32 kernel on 1-wave workgroups.)
 struct WaveDesc {
   int32_t item;
   int32_t tok_lo;   // first context position of the range
@@ -38,6 +38,12 @@ constexpr int kTileTokens = 32;   // tokens per inner-loop tile
 // (kMaxUnitTokens + 3 * 32) / 16 + 1 entries for 16-token blocks) is staged
 // in a 1040-entry LDS table by the bf16 kernel.
 constexpr int kMaxUnitTokens = 16384;
+// Upper bound of the shortest piece the planner cuts from a longer range, and
+// the start-up cost of a unit in tokens of streaming (per-unit loads of the
+// query rows and block table, and the refill of the load pipeline), used to
+// balance the workgroups' lists.
+constexpr int kMinPieceTokens = 512;
+constexpr int kUnitOverheadTokens = 256;
 constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, workgroups dealt round-robin
 
 }  // namespace spork

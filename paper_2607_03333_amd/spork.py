@@ -50,8 +50,8 @@ class spork_shape(ctypes.Structure):
 
 class spork_plan_info(ctypes.Structure):
     _fields_ = [("n_threads", _c_i32), ("n_rows", _c_i32), ("n_groups", _c_i32),
-                ("n_items", _c_i32), ("n_waves", _c_i32), ("n_partials", _c_i32),
-                ("max_row_tiles", _c_i32), ("pad_", _c_i32),
+                ("n_items", _c_i32), ("n_units", _c_i32), ("n_partials", _c_i32),
+                ("max_row_tiles", _c_i32), ("attn_grid", _c_i32),
                 ("image_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
                 ("shared_tokens", _c_i64), ("private_tokens", _c_i64),
                 ("unique_kv_bytes", _c_i64), ("flat_kv_bytes", _c_i64)]
@@ -247,7 +247,7 @@ def spork_plan_destroy(plan):
 def spork_plan_get_info(plan):
     info = spork_plan_info()
     _check(lib().spork_plan_get_info(plan, ctypes.byref(info)))
-    return {name: getattr(info, name) for name, _ in spork_plan_info._fields_ if name != "pad_"}
+    return {name: getattr(info, name) for name, _ in spork_plan_info._fields_}
 
 
 def spork_plan_image(plan):

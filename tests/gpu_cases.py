@@ -107,7 +107,7 @@ def run_workload(wl, tag, pick=None, check_tables=True, repeat_check=True):
             compare_tables(wl, dw)
         for step in steps:
             say(f"[{tag}] step {step.index}: threads {len(step.spec.seqs)} rows {sum(step.spec.n_rows)} "
-                f"waves {step.info['n_waves']} row_tiles {step.info['max_row_tiles']}")
+                f"units {step.info['n_units']} grid {step.info['attn_grid']} row_tiles {step.info['max_row_tiles']}")
             step.poison()
             step.run()
             torch.cuda.synchronize()
@@ -115,14 +115,21 @@ def run_workload(wl, tag, pick=None, check_tables=True, repeat_check=True):
             if step.verify:
                 compare_accept(wl, step, tag=f"{tag} step {step.index}")
             if repeat_check:
-                first = step.out.clone()
+                # A second run from poisoned outputs. The split of a unit's
+                # chunks between the workgroups that work on it depends on
+                # timing, so outputs agree with the first run only up to fp32
+                # summation order: both runs must meet the oracle bound.
+                first = step.out.float().clone()
                 first_lse = step.lse.clone()
                 step.poison()
                 step.run()
                 torch.cuda.synchronize()
-                assert torch.equal(first.view(torch.int16) if first.dtype == torch.bfloat16 else first,
-                                   step.out.view(torch.int16) if first.dtype == torch.bfloat16 else step.out)
-                assert torch.equal(first_lse, step.lse)
+                compare_attention(wl, step, pick, tag=f"{tag} step {step.index} (repeat)")
+                tol = FP32_TOL if step.out.dtype == torch.float32 else BF16_TOL
+                assert float((first - step.out.float()).abs().max()) <= tol
+                assert float(((first_lse - step.lse).abs() / first_lse.abs().clamp_min(1.0)).max()) <= LSE_REL
+                if step.verify:
+                    compare_accept(wl, step, tag=f"{tag} step {step.index} (repeat)")
         return dw
     except Exception:
         dw.close()

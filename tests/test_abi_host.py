@@ -195,7 +195,7 @@ def test_plan_covers_every_output_once_per_token():
     info, img = _decode_image(p)
     raw = img.view(np.int32)
     # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, merge_ids
-    nw = info["n_waves"]
+    nw = info["n_units"]
     waves = raw[: nw * 6].reshape(nw, 6)
     off = -(-nw * 24 // 256) * 256 // 4
     items = raw[off: off + info["n_items"] * 6].reshape(-1, 6)
@@ -226,5 +226,74 @@ def test_plan_covers_every_output_once_per_token():
                     seen[lo:hi] += 1
                 assert seen[: pos + 1].min() == 1 and seen[: pos + 1].max() == 1
         row += n
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+@pytest.mark.parametrize("index,n_cu,shrink", [
+    (4, 256, dict(sessions=6, prefix=9000, suffix=("loguniform", 1, 2000))),
+    (4, 16, dict(sessions=16, prefix=20000, suffix=("loguniform", 1, 3000))),
+    (3, 16, dict(sessions=3, prefix=3000, vocab=1000)),
+    (2, 8, dict(sessions=4, prefix=700, suffix=("uniform", 1, 600))),
+    (0, 2, {}),
+])
+def test_plan_lists(index, n_cu, shrink):
+    """Decode the unit lists (the image's last section: list offsets into the
+    unit list). bf16 plans launch 2 persistent workgroups per compute unit
+    that share one list per compute unit; the lists are balanced to within
+    one short piece of the per-list share (token cost plus 256 per unit),
+    run longest unit first with the two row slices of a range adjacent, and
+    long ranges are cut on 32-token boundaries into pieces of at most 16384
+    tokens; fp32 plans run one unit per workgroup."""
+    wl = synth.make(index, **shrink)
+    c, p = _plan_for(wl, n_cu=n_cu)
+    info, img = _decode_image(p)
+    raw = img.view(np.int32)
+    nu, grid = info["n_units"], info["attn_grid"]
+    bf16 = wl.dtype == synth.BF16
+    assert grid == (2 * n_cu if bf16 else nu)
+    n_lists = n_cu if bf16 else nu
+    off = (info["image_bytes"] - (-(-(n_lists + 1) * 4 // 256) * 256)) // 4
+    wg_off = raw[off: off + n_lists + 1]
+    assert wg_off[0] == 0 and wg_off[-1] == nu and np.all(np.diff(wg_off) >= 0)
+    units = raw[: nu * 6].reshape(nu, 6)
+    real = units[:, 0] >= 0
+    lens = units[:, 2] - units[:, 1]
+    assert np.all(lens[real] > 0) and lens.max() <= 16384
+    r = units[real]
+    assert r[0, 5] == 0 and np.all(r[1:, 5] == r[:-1, 5] + r[:-1, 4])
+    assert info["n_partials"] == int(r[-1, 5] + r[-1, 4])
+    # pieces cut from one range (slice 0): contiguous, on tile boundaries,
+    # and (persistent lists) at least 64 tokens but the last
+    pieces = {}
+    for u in r:
+        if u[3] == 0:
+            pieces.setdefault(int(u[0]), []).append((int(u[1]), int(u[2])))
+    for item, ps in pieces.items():
+        ps.sort()
+        for (lo, hi), nxt in zip(ps, ps[1:]):
+            assert nxt[0] == hi and hi % 32 == 0 and (hi - lo >= 64 or not bf16)
+    if not bf16:
+        assert np.array_equal(wg_off, np.arange(nu + 1))
+        spork.spork_plan_destroy(p)
+        spork.spork_cache_destroy(c)
+        return
+    loads = np.zeros(n_lists, dtype=np.int64)
+    for x in range(n_lists):
+        q = units[wg_off[x]:wg_off[x + 1]]
+        ql = q[:, 2] - q[:, 1]
+        assert np.all(np.diff(ql) <= 0), "list not longest first"
+        loads[x] = int((ql + 256).sum())
+        i = 0
+        while i < len(q):  # the row slices of one piece follow each other, from row 0
+            assert q[i, 3] == 0
+            j = i + 1
+            while j < len(q) and tuple(q[j, :3]) == tuple(q[i, :3]):
+                assert q[j, 3] == q[j - 1, 3] + q[j - 1, 4]
+                j += 1
+            i = j
+    share = -(-int(loads.sum()) // n_lists)
+    longest_small = max([int(x + 256) * 2 for x in lens if int(x + 256) * 2 <= share // 2] or [0])
+    assert loads.max() <= share + max(2 * (512 + 256), longest_small), (loads.max(), share)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)

@@ -4,14 +4,18 @@ The whole batch runs through the C ABI; the oracle recomputes a sample of
 threads one by one (the first and last thread, the longest context, the
 shortest private range, and a verify thread where there is one), element by
 element. Argmax and accept are compared on every row, bit-exactly, against
-the oracle and against the generator's planted values.
+the oracle and against the generator's planted values. Every output is also
+checked by a second run: which workgroup computes which chunk of a unit
+changes from run to run, so a chunk lost or counted twice anywhere in the
+batch shows up as a difference between the runs (they may differ only by
+fp32 summation order).
 """
 import numpy as np
 import pytest
 import torch
 
 from paper_2607_03333_amd import runner, synth
-from gpu_cases import compare_accept, compare_attention, say
+from gpu_cases import BF16_TOL, FP32_TOL, LSE_REL, compare_accept, compare_attention, say
 
 pytestmark = pytest.mark.gpu
 
@@ -41,11 +45,21 @@ def test_full_size_workload(index):
             step.run()
             torch.cuda.synchronize()
             pick = _pick(wl, step.index)
-            say(f"[full {wl.name}] step {step.index}: {step.info['n_waves']} workgroups, checking threads {pick}")
+            say(f"[full {wl.name}] step {step.index}: {step.info['n_units']} units on {step.info['attn_grid']} workgroups, checking threads {pick}")
             compare_attention(wl, step, set(pick), tag=f"full {wl.name} step {step.index}")
-            out = step.out.float()
+            out = step.out.float().clone()
+            lse = step.lse.clone()
             assert bool(torch.isfinite(out).all()), "non-finite outputs"
             if step.verify:
                 compare_accept(wl, step, tag=f"full {wl.name} step {step.index}")
+            step.poison()
+            step.run()
+            torch.cuda.synchronize()
+            tol = FP32_TOL if step.out.dtype == torch.float32 else BF16_TOL
+            d_out = float((out - step.out.float()).abs().max())
+            d_lse = float(((lse - step.lse).abs() / lse.abs().clamp_min(1.0)).max())
+            say(f"  full {wl.name} step {step.index}: all {out.shape[0]} x {out.shape[1]} outputs, run vs run: "
+                f"max-abs {d_out:.3e} lse-rel {d_lse:.3e}")
+            assert d_out <= tol and d_lse <= LSE_REL
     finally:
         dw.close()
