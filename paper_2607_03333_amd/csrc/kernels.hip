@@ -344,7 +344,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   const int taken = __builtin_amdgcn_readfirstlane(next_unit);
   if (taken >= list_len) break;
   const WaveDesc w = a.waves[list0 + taken];
-  if (w.item < 0) continue;
+  if (w.item < 0) {  // padding (not emitted on persistent lists): every wave reads next_unit first
+    __syncthreads();
+    continue;
+  }
   const ItemDesc it = a.items[w.item];
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
