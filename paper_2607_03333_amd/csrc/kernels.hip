@@ -228,7 +228,8 @@ __global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) { accept_unit(
 // --------------------------------------------------------------------------
 // bf16 partial attention. A persistent workgroup of 4 waves works through its
 // list of units; a unit is a token range of one work item and up to 4*RTW
-// 16-row tiles of its query rows; wave w computes tiles w, w+4, ... . The range streams through a ring of kRing LDS slots, one
+// 16-row tiles of its query rows; wave w computes tiles c, c+4 (c = w, or w + 2
+// mod 4 in the second workgroup of a compute unit). The range streams through a ring of kRing LDS slots, one
 // 32-token K/V tile ("stage", 16 KB) each, filled by direct global-to-LDS
 // 16-byte loads (global_load_lds_dwordx4: lane i of an instruction lands at
 // the instruction's LDS base + 16*i), so kRing-1 stages stay in flight without
@@ -236,10 +237,14 @@ __global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) { accept_unit(
 // half, waves 2-3 the V half); one barrier per stage publishes a slot to all
 // waves and frees the slot read in the previous stage.
 //
-// LDS slot layout (1024 chunks of 16 bytes, XOR-swizzled so that the MFMA
-// operand reads of each 8-lane group hit 8 different 128-byte bank groups):
+// LDS slot layout (1024 chunks of 16 bytes). Bank model (measured on
+// gfx950): 64 banks of 4 bytes, so a 16-byte slot s sits in bank group
+// s mod 16; a ds_read_b128 serves a wave in four groups of 16 lanes (half
+// lane >> 5, phase = parity of lane bits 2-4: lanes 0-3, 12-15, 20-27 |
+// 4-11, 16-19, 28-31 of each half), and inside a group distinct addresses
+// in one bank group serialise. Both operand reads below are conflict-free:
 //   K: chunk t*16 + (c ^ fk(t)) holds channels 8c..8c+7 of tile token t,
-//      fk(t) = (t & 3) | ((t >> 1) & 4);
+//      fk(t) = (t & 3) | ((t >> 1) & 12);
 //   V: chunk 512 + d*4 + (q ^ ((d >> 1) & 3)) holds tokens 8q..8q+7 of
 //      channel d (from the channel-major V blocks).
 //
@@ -258,11 +263,12 @@ constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 by
 constexpr int kRing = 4;            // LDS stages per workgroup (kRing - 1 in flight)
 constexpr int kUnitBlocks = 1040;   // block-table entries a unit may span (see kMaxUnitTokens)
 constexpr float kRescaleSlack = 8.0f;  // base-2 headroom before the reference max moves
+constexpr float kRescaleSum = 256.0f;  // 2^kRescaleSlack: bound on a lane's 8 probabilities of a row
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 typedef __attribute__((address_space(1))) void* global_void_ptr;
 
-__device__ __forceinline__ int k_swz(int t) { return (t & 3) | ((t >> 1) & 4); }
+__device__ __forceinline__ int k_swz(int t) { return (t & 3) | ((t >> 1) & 12); }
 __device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
 
 // Zero the bf16 lanes of an 8-token chunk starting at position `first` whose
@@ -350,6 +356,12 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   }
   const ItemDesc it = a.items[w.item];
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  // Row tiles go to waves by `cw`, the wave index rotated by two in the
+  // second workgroup of a compute unit (workgroups b and b + n_lists share
+  // one): wave w of both shares SIMD w, and with 5-7 tiles (two for some
+  // waves, one for others) the rotation pairs each wave holding two tiles
+  // with one holding one.
+  const int cw = (wave + 2 * (static_cast<int>(blockIdx.x) / a.n_lists)) & (kWgWaves - 1);
   const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ qg = static_cast<const uint16_t*>(a.q);
   const uint16_t* __restrict__ kc = static_cast<const uint16_t*>(a.k_cache);
@@ -366,7 +378,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   bool own[RTW];
 #pragma unroll
   for (int j = 0; j < RTW; ++j) {
-    const int tile = wave + kWgWaves * j;
+    const int tile = cw + kWgWaves * j;
     own[j] = tile < ntiles;
     const int i = tile * 16 + r16;
     if (own[j] && i < w.nrows) {
@@ -472,9 +484,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
 
   // Softmax in base 2 with a lazily moved reference max: scores enter as
   // p = 2^(s*c - m) with m the row's reference; m (and the accumulator, by
-  // 2^(m_old - m_new)) moves only when a score exceeds m + kRescaleSlack, so
-  // p <= 2^kRescaleSlack and most stages skip the rescale. The merge only
-  // needs (m, l, o) to be consistent, not m to be the exact maximum.
+  // 2^(m_old - m_new)) moves only when a lane's probabilities of the row sum
+  // past 2^kRescaleSlack, so p <= 2^kRescaleSlack and most stages skip the
+  // rescale. The merge only needs (m, l, o) to be consistent, not m to be the
+  // exact maximum.
   const float c = a.scale_log2;
   // One stage for NT owned tiles, reading ring slot (st % kRing).
   auto compute_tiles = [&](auto nt_c, int st) __attribute__((always_inline)) {
@@ -519,13 +532,25 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
           if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[e] = kNegInf;
         }
       }
-      // Common case: every score is within kRescaleSlack of the row's
-      // reference, checked lane by lane; only when some lane of the wave sees
-      // a larger score are the row maxima reduced across lanes and the
-      // reference moved (rows that did not trigger keep theirs).
-      float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])), fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
-      mx *= c;
-      if (__ballot(mx > m[j] + kRescaleSlack) != 0) {
+      // Common case: the lane's 8 probabilities of the row, taken against
+      // the row's reference, sum to at most 2^kRescaleSlack (which bounds
+      // each of them). Only when some lane of the wave sums past that, or a
+      // row has no reference yet, are the row maxima reduced across lanes,
+      // the reference moved where it lags by more than kRescaleSlack (rows
+      // that did not trigger keep theirs) and the probabilities recomputed.
+      float ps = 0.0f;
+      float pv[8];
+      {
+        const float mu = m[j] == kNegInf ? 0.0f : m[j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
+          ps += pv[e];
+        }
+      }
+      if (__ballot(!(ps <= kRescaleSum) || m[j] == kNegInf) != 0) {
+        float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])), fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+        mx *= c;
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         if (mx > m[j] + kRescaleSlack) {  // row-uniform: all 4 lanes of the row agree
@@ -535,16 +560,16 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
           for (int dt = 0; dt < 8; ++dt) o[j][dt] *= alpha;
           m[j] = mx;
         }
-      }
-      const float mu = m[j] == kNegInf ? 0.0f : m[j];
-      float ps = 0.0f;
+        const float mu = m[j] == kNegInf ? 0.0f : m[j];
+        ps = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
-        ps += sv[e];
+        for (int e = 0; e < 8; ++e) {
+          pv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
+          ps += pv[e];
+        }
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pop[j][e] = static_cast<__bf16>(sv[e]);
+      for (int e = 0; e < 8; ++e) pop[j][e] = static_cast<__bf16>(pv[e]);
       l[j] += ps;
     }
     lds_wait(vr);
@@ -593,7 +618,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
     for (int j = 0; j < NT; ++j) {
       float lt = l[j] + __shfl_xor(l[j], 16);
       lt += __shfl_xor(lt, 32);
-      const int i = (wave + kWgWaves * j) * 16 + r16;
+      const int i = (cw + kWgWaves * j) * 16 + r16;
       if (i < w.nrows) {
         const size_t pr = static_cast<size_t>(w.partial + i);
         if (g == 0) {
