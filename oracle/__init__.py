@@ -15,6 +15,8 @@ paper it follows (SPORK, arXiv 2607.03333):
   (Section 4.3, step 2; greedy decoding, Section 6.1 "Setup").
 * argmax + accept: greedy target tokens and the longest draft prefix that
   matches them (Section 4.3, steps 2-3; Appendix B).
+* confidence: the top-1 log-probability of each probe position and the D2
+  gate over the tool-name span (Section 4.2).
 
 Parity status of each function is stated in its module header.
 """
@@ -23,8 +25,10 @@ from .block_manager import BlockManager, NoBlocksError
 from .kv import scatter_tokens, gather_context
 from .attention import attend, attend_batch
 from .accept import argmax_rows, accept_drafts
+from .confidence import top1_logprob, span_confidence, confidence_gate
 
 __all__ = [
     "BlockManager", "NoBlocksError", "scatter_tokens", "gather_context",
     "attend", "attend_batch", "argmax_rows", "accept_drafts",
+    "top1_logprob", "span_confidence", "confidence_gate",
 ]
