@@ -33,12 +33,17 @@ METRIC = "forked decode-attn unique-KV GB/s (% of 8 TB/s) + verified tokens/s"
 HBM_PEAK_GBPS = 8000.0
 DEFAULT_WORKLOAD = "qwen3-30b-a3b-mixed"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_partial_traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_03333_amd", "csrc", "kernels.hip")
+# the attention kernel's source and every header it includes
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_03333_amd", "csrc", f)
+                  for f in ("attention.hip", "device_common.h", "kernels.h", "plan_types.h")]
 
 
 def kernel_source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload):
@@ -100,6 +105,57 @@ def cpu_baseline(wl, step_specs, target_s):
                       f"in {dt:.1f} s, float64 NumPy, {os.cpu_count()} logical CPUs visible"}
 
 
+def confidence_bench(args, torch, spork, synth):
+    """D2 confidence gate alone: one JSON line, HBM roofline of the chunk pass
+    (2 bytes per bf16 logit read once)."""
+    vocab = 151936
+    b = synth.probe_batch(args.confidence_probes, vocab, dtype=synth.BF16, span=(0, 16), seed=1)
+    rows = b.logits.shape[0]
+    dev = torch.device("cuda:0")
+    x = torch.from_numpy(b.logits.view("int16")).to(dev).view(torch.bfloat16)
+    off = torch.from_numpy(b.span_off).to(dev)
+    am = torch.empty(rows, dtype=torch.int32, device=dev)
+    lp = torch.empty(rows, dtype=torch.float32, device=dev)
+    conf = torch.empty(args.confidence_probes, dtype=torch.float32, device=dev)
+    commit = torch.empty(args.confidence_probes, dtype=torch.int32, device=dev)
+    ws = torch.empty(spork.spork_confidence_workspace_bytes(rows, vocab), dtype=torch.uint8, device=dev)
+
+    def step():
+        spork.spork_probe_confidence(x, spork.SPORK_DTYPE_BF16, vocab, rows, off, args.confidence_probes,
+                                     0.90, am, lp, conf, commit, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spork.spork_timing_read()
+    spork.spork_timing_enable(True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    spork.spork_timing_enable(False)
+    kern = spork.spork_timing_read()
+    ms_step = start.elapsed_time(end) / args.steps
+    nbytes = rows * vocab * 2
+    ms_chunks = kern["conf_chunks"][0] / max(kern["conf_chunks"][1], 1)
+    achieved = nbytes / (ms_chunks * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "D2 confidence gate: logits GB/s", "value": round(nbytes / (ms_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded Gaussian logits with a boosted top-1 token)",
+        "config": {"workload": "probe-confidence", "probes": args.confidence_probes, "rows": rows,
+                   "vocab": vocab, "theta": 0.90},
+        "kernel_ms_per_step": {k: round(v[0] / max(v[1], 1), 4) for k, v in kern.items() if v[1]},
+        "commits": int(commit.sum().item()),
+        "roofline": {"bound": "hbm", "kernel": "conf_chunks", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_launch_ms": round(ms_chunks, 4), "algorithmic_bytes_per_launch": nbytes}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,6 +167,9 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="instead of the benchmark, run one plain device copy of this many MiB "
                          "(reference kernel for the HBM traffic counters) and exit")
+    ap.add_argument("--confidence-probes", type=int, default=0,
+                    help="instead of the benchmark, time the D2 confidence gate over this many probe "
+                         "spans (0..16 positions each) of the 151,936-token vocabulary, bf16 logits")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -136,6 +195,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n}), flush=True)
+        return
+
+    if args.confidence_probes:
+        confidence_bench(args, torch, spork, synth)
         return
 
     t_gen = time.perf_counter()

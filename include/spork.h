@@ -16,6 +16,10 @@
  *     drafts; the greedy token of every verify row is the lowest index of its
  *     row maximum, and the accepted length is the longest draft prefix that
  *     equals the greedy tokens (decoding resumes after the first mismatch).
+ *   - spork_probe_confidence: design D2's gate (Section 4.2): the top-1
+ *     log-probability of every probe position and, per probe, the smallest
+ *     top-1 probability over its tool-name span without the span's first
+ *     token, compared with a threshold.
  *
  * Conventions
  *   - Every entry point returns SPORK_OK (0) or a negative status and never
@@ -229,6 +233,35 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
                         int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
                         void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* Workspace for spork_probe_confidence. */
+int spork_confidence_workspace_bytes(int32_t n_rows, int32_t vocab, size_t* bytes);
+
+/* D2 confidence gate (Section 4.2, confidence score).
+ * logits (device [n_rows][vocab], logits_dtype f32 or bf16): one row per
+ * generated probe position; every row needs a finite maximum (-inf entries
+ * are allowed, NaN is not). span_off (device int32 [n_probes+1],
+ * non-decreasing, within [0, n_rows]): probe p's tool-name span is rows
+ * span_off[p] .. span_off[p+1]-1; offsets are clamped to [0, n_rows] and a
+ * reversed span counts as empty, so bad offsets never read out of bounds.
+ * Outputs (device): argmax_out[n_rows] int32 (nullable) = greedy token, the
+ *   lowest index of the row maximum; logprob_out[n_rows] float32 (nullable)
+ *   = top-1 log-probability max(x) - ln(sum exp(x)), accumulated in float32;
+ *   confidence_out[n_probes] float32 = min over the span's rows after the
+ *   first of exp(logprob), 1.0 for a span of fewer than two rows;
+ *   commit_out[n_probes] int32 (nullable) = confidence_out >= theta, decided
+ *   in float32.
+ * workspace (device, 256-byte aligned, ws_bytes >= the size from
+ * spork_confidence_workspace_bytes; any contents on entry).
+ * Two launches on `stream`: per-chunk argmax and sum of exponentials, then
+ * per-row results and the per-probe gate. SPORK_E_INVAL for bad sizes or a
+ * NULL required pointer, SPORK_E_UNSUPPORTED for another logits dtype,
+ * SPORK_E_CAPACITY for a short workspace. */
+int spork_probe_confidence(const void* logits, int32_t logits_dtype, int32_t vocab,
+                           int32_t n_rows, const int32_t* span_off, int32_t n_probes,
+                           float theta, int32_t* argmax_out, float* logprob_out,
+                           float* confidence_out, int32_t* commit_out, void* workspace,
+                           size_t ws_bytes, hipStream_t stream);
+
 /* ======================================================================== *
  *  Kernel timing (benchmarks).
  * ======================================================================== */
@@ -236,7 +269,9 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
 #define SPORK_KERNEL_MERGE 1  /* log-sum-exp merge (+ the verify step's accept) */
 #define SPORK_KERNEL_ARGMAX 2 /* greedy argmax over vocabulary chunks */
 #define SPORK_KERNEL_ACCEPT 3 /* accept of an accept-only call (plan == NULL) */
-#define SPORK_KERNEL_KINDS 4
+#define SPORK_KERNEL_CONF_CHUNKS 4 /* confidence: per-chunk argmax and sum of exponentials */
+#define SPORK_KERNEL_CONF_FINAL 5  /* confidence: per-row log-probability and per-probe gate */
+#define SPORK_KERNEL_KINDS 6
 
 /* While enabled (per calling thread), every hot-path call records a HIP event
  * before and after each of its kernels on the caller's stream. */

@@ -1,4 +1,4 @@
-// gfx950 (MI355X, CDNA4) kernels of the forked-decode hot path.
+// gfx950 (MI355X, CDNA4) attention kernels of the forked-decode hot path.
 //
 //  * attn_bf16 / attn_f32: partial attention of one work item's token range
 //    for up to RT 16-row tiles of query rows (split-K). A work item is either
@@ -9,62 +9,12 @@
 //    accumulation; K and V stream from HBM with 16-byte loads straight into
 //    the MFMA operand registers.
 //  * merge: log-sum-exp merge of an output row's partials (DPP wave
-//    reductions), written in the input dtype, plus the row's lse.
-//  * argmax_chunks + accept: greedy token of every verify row (lowest index of
-//    the row maximum) and the longest draft prefix equal to the greedy tokens
-//    (Section 4.3, steps 2-3).
-//  * kv_write / kv_copy: token scatter into the paged pools and the copy of
-//    copy-on-write (setup work, not on the timed path).
-#include <hip/hip_runtime.h>
-
-#include <climits>
-#include <cstdint>
-#include <type_traits>
-
-#include "kernels.h"
+//    reductions), written in the input dtype, plus the row's lse; the same
+//    launch runs the accept of a verify step (Section 4.3, steps 2-3).
+#include "device_common.h"
 
 namespace spork {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr float kNegInf = -__builtin_huge_valf();
-constexpr float kLn2 = 0.693147180559945309f;
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// --------------------------------------------------------------------------
-// Wave-wide reductions with DPP: butterflies inside each 16-lane row
-// (quad permutes, half-row and row mirrors), then the row broadcasts 15 and
-// 31 carry the partial results across rows; lane 63 ends with the total.
-// --------------------------------------------------------------------------
-template <int kCtrl, int kRowMask>
-__device__ __forceinline__ float dpp_mov(float ident, float x) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, ident), __builtin_bit_cast(int, x),
-                                         kCtrl, kRowMask, 0xF, false));
-}
-
-template <typename Op>
-__device__ __forceinline__ float wave_reduce(float x, float ident, Op op) {
-  x = op(x, dpp_mov<0xB1, 0xF>(ident, x));   // quad_perm [1,0,3,2]
-  x = op(x, dpp_mov<0x4E, 0xF>(ident, x));   // quad_perm [2,3,0,1]
-  x = op(x, dpp_mov<0x141, 0xF>(ident, x));  // row_half_mirror
-  x = op(x, dpp_mov<0x140, 0xF>(ident, x));  // row_mirror
-  x = op(x, dpp_mov<0x142, 0xA>(ident, x));  // row_bcast:15 into rows 1 and 3
-  x = op(x, dpp_mov<0x143, 0xC>(ident, x));  // row_bcast:31 into rows 2 and 3
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
-}
-
-__device__ __forceinline__ float wave_max(float x) {
-  return wave_reduce(x, kNegInf, [](float a, float b) { return fmaxf(a, b); });
-}
-__device__ __forceinline__ float wave_sum(float x) {
-  return wave_reduce(x, 0.0f, [](float a, float b) { return a + b; });
-}
 
 // --------------------------------------------------------------------------
 // Online softmax step shared by both attention kernels. `sv` holds this
@@ -92,138 +42,6 @@ __device__ __forceinline__ float softmax_step(float (&sv)[8], float& m, float& l
   m = mn;
   return alpha;
 }
-
-__device__ __forceinline__ int wave_min_int(int x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = min(x, __shfl_xor(x, o));
-  return x;
-}
-
-// --------------------------------------------------------------------------
-// Greedy argmax, first pass: the best (value, index) of one chunk of a row.
-// Each thread scans its elements in increasing index order keeping the first
-// strict maximum; chunks and threads combine through the 64-bit key
-// (order-preserving value bits << 32) | (0xFFFFFFFF - index), whose maximum
-// is the largest value at the lowest index. -0 is keyed as +0.
-// --------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t argmax_key(float v, int idx) {
-  if (idx == INT_MAX) return 0;
-  uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(idx));
-}
-
-__device__ __forceinline__ float load_f(const float* p, int i) { return p[i]; }
-__device__ __forceinline__ float load_f(const uint16_t* p, int i) {
-  return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
-}
-
-// One (row, chunk) argmax unit run by a workgroup of NT threads; writes the
-// chunk's key to keys[row * chunks + chunk].
-template <typename T, int NT>
-__device__ __forceinline__ void argmax_unit(const AcceptArgs& a, int unit) {
-  constexpr int VEC = 16 / sizeof(T);
-  constexpr int NW = NT / 64;
-  const int row = unit / a.chunks, c = unit % a.chunks;
-  const T* x = static_cast<const T*>(a.logits) + static_cast<size_t>(row) * a.vocab;
-  float best = kNegInf;
-  int bidx = INT_MAX;
-  const bool vec_ok = (a.vocab % VEC) == 0 && (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0;
-  if (vec_ok) {
-    const int nv = a.vocab / VEC;
-    const int lo = static_cast<int>(static_cast<int64_t>(nv) * c / a.chunks);
-    const int hi = static_cast<int>(static_cast<int64_t>(nv) * (c + 1) / a.chunks);
-    const uint4* xv = reinterpret_cast<const uint4*>(x);
-    auto scan = [&](const uint4& u, int v) __attribute__((always_inline)) {
-      const T* e = reinterpret_cast<const T*>(&u);
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) {
-        const float val = load_f(e, j);
-        if (val > best || bidx == INT_MAX) {
-          best = val;
-          bidx = v * VEC + j;
-        }
-      }
-    };
-    // four 16-byte loads in flight per thread, scanned in index order
-    int v = lo + static_cast<int>(threadIdx.x);
-    for (; v + 3 * NT < hi; v += 4 * NT) {
-      const uint4 u0 = xv[v], u1 = xv[v + NT], u2 = xv[v + 2 * NT], u3 = xv[v + 3 * NT];
-      scan(u0, v);
-      scan(u1, v + NT);
-      scan(u2, v + 2 * NT);
-      scan(u3, v + 3 * NT);
-    }
-    for (; v < hi; v += NT) scan(xv[v], v);
-  } else {
-    const int lo = static_cast<int>(static_cast<int64_t>(a.vocab) * c / a.chunks);
-    const int hi = static_cast<int>(static_cast<int64_t>(a.vocab) * (c + 1) / a.chunks);
-    for (int i = lo + static_cast<int>(threadIdx.x); i < hi; i += NT) {
-      const float val = load_f(x, i);
-      if (val > best || bidx == INT_MAX) {
-        best = val;
-        bidx = i;
-      }
-    }
-  }
-  uint64_t key = argmax_key(best, bidx);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const uint64_t other = __shfl_xor(key, o);
-    key = other > key ? other : key;
-  }
-  if constexpr (NW > 1) {
-    __shared__ uint64_t wk[NW];
-    if ((threadIdx.x & 63) == 0) wk[threadIdx.x >> 6] = key;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint64_t k = wk[0];
-      for (int i = 1; i < NW; ++i) k = wk[i] > k ? wk[i] : k;
-      a.keys[static_cast<size_t>(row) * a.chunks + c] = k;
-    }
-  } else {
-    if (threadIdx.x == 0) a.keys[static_cast<size_t>(row) * a.chunks + c] = key;
-  }
-}
-
-template <typename T>
-__global__ void __launch_bounds__(256) argmax_chunks(AcceptArgs a) {
-  if (a.counters != nullptr)
-    for (int i = blockIdx.x * 256 + threadIdx.x; i < a.n_counters; i += gridDim.x * 256) a.counters[i] = 0;
-  argmax_unit<T, 256>(a, blockIdx.x);
-}
-
-// Accept for verify thread s, run by one wave: combine the chunk keys of its
-// K+1 rows (lane r handles rows r, r+64, ...), then the first draft that
-// differs from the greedy token ends the accepted prefix (a ballot per 64 rows).
-__device__ __forceinline__ int greedy_of(const AcceptArgs& a, int row) {
-  const uint64_t* kp = a.keys + static_cast<size_t>(row) * a.chunks;
-  uint64_t best = 0;
-  for (int c = 0; c < a.chunks; ++c) best = kp[c] > best ? kp[c] : best;
-  return static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(best));
-}
-
-__device__ __forceinline__ void accept_unit(const AcceptArgs& a, int s) {
-  const int lane = threadIdx.x & 63, kd = a.k_drafts;
-  int first = kd;
-  for (int base = 0; base <= kd; base += 64) {
-    const int r = base + lane;
-    bool miss = false;
-    if (r <= kd) {
-      const int g = greedy_of(a, s * (kd + 1) + r);
-      if (a.argmax_out != nullptr) a.argmax_out[s * (kd + 1) + r] = g;
-      miss = r < kd && g != a.drafts[static_cast<size_t>(s) * kd + r];
-    }
-    const uint64_t bal = __ballot(miss);
-    if (bal != 0 && first == kd) first = base + __builtin_ctzll(bal);
-  }
-  if (lane == 0) {
-    a.accept_len[s] = first;
-    a.next_token[s] = greedy_of(a, s * (kd + 1) + first);
-  }
-}
-
-__global__ void __launch_bounds__(64) accept_kernel(AcceptArgs a) { accept_unit(a, blockIdx.x); }
 
 // --------------------------------------------------------------------------
 // bf16 partial attention. A persistent workgroup of 4 waves works through its
@@ -874,51 +692,6 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     a.lse[o] = sum > 0.0f ? (mu + __log2f(sum)) * kLn2 : kNegInf;
 }
 
-// --------------------------------------------------------------------------
-// Setup kernels.
-// --------------------------------------------------------------------------
-template <typename T>
-__global__ void __launch_bounds__(256) kv_write_kernel(int hkv, int D, int BS, int64_t num_slots, T* kc,
-                                                       T* vc, const int64_t* slots, const T* kn,
-                                                       const T* vn, int n, int* bad) {
-  constexpr int VEC = 16 / sizeof(T);
-  const int per_tok = hkv * (D / VEC);
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (idx >= static_cast<int64_t>(n) * per_tok) return;
-  const int i = static_cast<int>(idx / per_tok);
-  const int rem = static_cast<int>(idx % per_tok);
-  const int h = rem / (D / VEC), cchunk = rem % (D / VEC);
-  const int64_t slot = slots[i];
-  if (slot < 0 || slot >= num_slots) {
-    if (rem == 0 && bad != nullptr) atomicAdd(bad, 1);
-    return;
-  }
-  const int64_t b = slot / BS, off = slot % BS;
-  const size_t src = (static_cast<size_t>(i) * hkv + h) * D + static_cast<size_t>(cchunk) * VEC;
-  *reinterpret_cast<uint4*>(kc + ((static_cast<size_t>(b) * hkv + h) * BS + off) * D + cchunk * VEC) =
-      *reinterpret_cast<const uint4*>(kn + src);
-  const T* vs = vn + src;
-  T* vd = vc + (static_cast<size_t>(b) * hkv + h) * static_cast<size_t>(D) * BS + off;
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) vd[static_cast<size_t>(cchunk * VEC + e) * BS] = vs[e];
-}
-
-template <typename T>
-__global__ void __launch_bounds__(256) kv_copy_kernel(int hkv, int D, int BS, T* kc, T* vc, int src, int dst,
-                                                      int nv) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (idx >= static_cast<int64_t>(hkv) * nv * D) return;
-  const int h = static_cast<int>(idx / (static_cast<int64_t>(nv) * D));
-  const int rem = static_cast<int>(idx % (static_cast<int64_t>(nv) * D));
-  const int off = rem / D, d = rem % D;
-  const size_t ks = ((static_cast<size_t>(src) * hkv + h) * BS + off) * D + d;
-  const size_t kd = ((static_cast<size_t>(dst) * hkv + h) * BS + off) * D + d;
-  kc[kd] = kc[ks];
-  const size_t vs = ((static_cast<size_t>(src) * hkv + h) * D + d) * BS + off;
-  const size_t vd = ((static_cast<size_t>(dst) * hkv + h) * D + d) * BS + off;
-  vc[vd] = vc[vs];
-}
-
 __global__ void __launch_bounds__(256) counter_reset_kernel(int32_t* counters, int32_t n) {
   for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) counters[i] = 0;
 }
@@ -994,63 +767,6 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL((merge_kernel<64, float>), dim3(blocks), dim3(256), 0, stream, a);
   else
     return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-int32_t accept_chunks(int32_t rows, int32_t vocab) {
-  const int32_t max_chunks = vocab / (256 * 8 * 4) > 1 ? vocab / (256 * 8 * 4) : 1;
-  int32_t c = rows > 0 ? (2048 + rows - 1) / rows : 1;
-  if (c > max_chunks) c = max_chunks;
-  return c < 1 ? 1 : c;
-}
-
-hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream) {
-  const int rows = a.n_verify * (a.k_drafts + 1);
-  if (rows == 0) return hipSuccess;
-  if (a.logits_dtype == 1)
-    hipLaunchKernelGGL(argmax_chunks<uint16_t>, dim3(rows * a.chunks), dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(argmax_chunks<float>, dim3(rows * a.chunks), dim3(256), 0, stream, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_accept_tail(const AcceptArgs& a, hipStream_t stream) {
-  if (a.n_verify == 0) return hipSuccess;
-  hipLaunchKernelGGL(accept_kernel, dim3(a.n_verify), dim3(64), (a.k_drafts + 1) * sizeof(int), stream, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_kv_write(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
-                           int64_t num_slots, void* k_cache, void* v_cache, const int64_t* slots,
-                           const void* k_new, const void* v_new, int32_t n, int32_t* bad_slots,
-                           hipStream_t stream) {
-  if (n == 0) return hipSuccess;
-  const int vec = dtype == 1 ? 8 : 4;
-  const int64_t total = static_cast<int64_t>(n) * hkv * (head_dim / vec);
-  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
-  if (dtype == 1)
-    hipLaunchKernelGGL(kv_write_kernel<uint16_t>, grid, dim3(256), 0, stream, hkv, head_dim, block_size, num_slots,
-                       static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), slots,
-                       static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), n, bad_slots);
-  else
-    hipLaunchKernelGGL(kv_write_kernel<float>, grid, dim3(256), 0, stream, hkv, head_dim, block_size, num_slots,
-                       static_cast<float*>(k_cache), static_cast<float*>(v_cache), slots,
-                       static_cast<const float*>(k_new), static_cast<const float*>(v_new), n, bad_slots);
-  return hipGetLastError();
-}
-
-hipError_t launch_kv_copy(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
-                          void* k_cache, void* v_cache, int32_t src, int32_t dst, int32_t n_valid,
-                          hipStream_t stream) {
-  if (n_valid == 0) return hipSuccess;
-  const int64_t total = static_cast<int64_t>(hkv) * n_valid * head_dim;
-  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
-  if (dtype == 1)
-    hipLaunchKernelGGL(kv_copy_kernel<uint16_t>, grid, dim3(256), 0, stream, hkv, head_dim, block_size,
-                       static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), src, dst, n_valid);
-  else
-    hipLaunchKernelGGL(kv_copy_kernel<float>, grid, dim3(256), 0, stream, hkv, head_dim, block_size,
-                       static_cast<float*>(k_cache), static_cast<float*>(v_cache), src, dst, n_valid);
   return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@
 
 #include "block_manager.h"
 #include "kernels.h"
+#include "vocab_kernels.h"
 #include "plan.h"
 
 struct spork_cache {
@@ -440,6 +441,58 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     if (rc != SPORK_OK) return rc;
     return hip_status(timed(SPORK_KERNEL_ACCEPT, stream, [&] { return spork::launch_accept_tail(a, stream); }),
                       "spork_verify_accept (accept)");
+  });
+}
+
+int spork_confidence_workspace_bytes(int32_t n_rows, int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return fail(SPORK_E_INVAL, "bytes is NULL");
+  if (n_rows < 0 || vocab <= 0) return fail(SPORK_E_INVAL, "n_rows >= 0 and vocab > 0 required");
+  // per (row, chunk): the argmax key and the (max, sum) pair
+  *bytes = static_cast<size_t>(n_rows) * spork::accept_chunks(n_rows, vocab) * (sizeof(uint64_t) + 2 * sizeof(float));
+  return SPORK_OK;
+}
+
+int spork_probe_confidence(const void* logits, int32_t logits_dtype, int32_t vocab, int32_t n_rows,
+                           const int32_t* span_off, int32_t n_probes, float theta, int32_t* argmax_out,
+                           float* logprob_out, float* confidence_out, int32_t* commit_out, void* workspace,
+                           size_t ws_bytes, hipStream_t stream) {
+  return guarded([&] {
+    if (n_rows < 0 || n_probes < 0 || vocab <= 0)
+      return fail(SPORK_E_INVAL, "n_rows >= 0, n_probes >= 0 and vocab > 0 required");
+    if (logits_dtype != SPORK_DTYPE_F32 && logits_dtype != SPORK_DTYPE_BF16)
+      return fail(SPORK_E_UNSUPPORTED, "logits dtype must be f32 or bf16");
+    if (static_cast<int64_t>(n_rows) * vocab > (static_cast<int64_t>(1) << 40))
+      return fail(SPORK_E_INVAL, "logits too large");
+    if (n_rows > 0 && logits == nullptr) return fail(SPORK_E_INVAL, "logits is NULL");
+    if (n_probes > 0 && (span_off == nullptr || confidence_out == nullptr))
+      return fail(SPORK_E_INVAL, "span_off and confidence_out are required when n_probes > 0");
+    size_t need = 0;
+    spork_confidence_workspace_bytes(n_rows, vocab, &need);
+    if (ws_bytes < need) return fail(SPORK_E_CAPACITY, "workspace too small");
+    if (need > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
+      return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
+    spork::ConfArgs a{};
+    a.logits = logits;
+    a.logits_dtype = logits_dtype;
+    a.vocab = vocab;
+    a.n_rows = n_rows;
+    a.chunks = spork::accept_chunks(n_rows, vocab);
+    a.n_probes = n_probes;
+    a.span_off = span_off;
+    a.theta = theta;
+    a.argmax_out = argmax_out;
+    a.logprob_out = logprob_out;
+    a.confidence_out = confidence_out;
+    a.commit_out = commit_out;
+    const size_t units = static_cast<size_t>(n_rows) * a.chunks;
+    a.keys = static_cast<uint64_t*>(workspace);
+    a.ms = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + units * sizeof(uint64_t));
+    const int rc = hip_status(
+        timed(SPORK_KERNEL_CONF_CHUNKS, stream, [&] { return spork::launch_conf_chunks(a, stream); }),
+        "spork_probe_confidence (chunks)");
+    if (rc != SPORK_OK) return rc;
+    return hip_status(timed(SPORK_KERNEL_CONF_FINAL, stream, [&] { return spork::launch_conf_final(a, stream); }),
+                      "spork_probe_confidence (final)");
   });
 }
 

@@ -27,8 +27,10 @@ SPORK_KERNEL_ATTN = 0
 SPORK_KERNEL_MERGE = 1
 SPORK_KERNEL_ARGMAX = 2
 SPORK_KERNEL_ACCEPT = 3
-SPORK_KERNEL_KINDS = 4
-KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept")
+SPORK_KERNEL_CONF_CHUNKS = 4
+SPORK_KERNEL_CONF_FINAL = 5
+SPORK_KERNEL_KINDS = 6
+KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept", "conf_chunks", "conf_final")
 
 _c_i32 = ctypes.c_int32
 _c_i64 = ctypes.c_int64
@@ -85,6 +87,10 @@ _SIGNATURES = {
                                                     ctypes.POINTER(ctypes.c_size_t)]),
     "spork_verify_accept": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _c_i32, _c_i32, _p,
                                            _c_i32, _c_i32, _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "spork_confidence_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i32,
+                                                        ctypes.POINTER(ctypes.c_size_t)]),
+    "spork_probe_confidence": (ctypes.c_int, [_p, _c_i32, _c_i32, _c_i32, _p, _c_i32, ctypes.c_float,
+                                              _p, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "spork_timing_enable": (ctypes.c_int, [_c_i32]),
     "spork_timing_read": (ctypes.c_int, [_p, _p]),
 }
@@ -279,6 +285,21 @@ def spork_verify_accept(plan, dev_image, q, k_cache, v_cache, out, lse, logits, 
                                      _ptr(drafts), n_verify, k_drafts, _ptr(accept_len),
                                      _ptr(next_token), _ptr(argmax_out), _ptr(workspace), ws_bytes,
                                      _stream(stream)))
+
+
+def spork_confidence_workspace_bytes(n_rows, vocab):
+    b = ctypes.c_size_t()
+    _check(lib().spork_confidence_workspace_bytes(n_rows, vocab, ctypes.byref(b)))
+    return b.value
+
+
+def spork_probe_confidence(logits, logits_dtype, vocab, n_rows, span_off, n_probes, theta,
+                           argmax_out, logprob_out, confidence_out, commit_out, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spork_probe_confidence(_ptr(logits), logits_dtype, vocab, n_rows, _ptr(span_off),
+                                        n_probes, float(theta), _ptr(argmax_out), _ptr(logprob_out),
+                                        _ptr(confidence_out), _ptr(commit_out), _ptr(workspace),
+                                        ws_bytes, _stream(stream)))
 
 
 # ---- kernel timing ------------------------------------------------------------

@@ -348,3 +348,40 @@ def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=No
         step.planted_accept = n_match
         step.planted_next = g[np.arange(n_ver), n_match]
     return wl
+
+
+@dataclass
+class ProbeBatch:
+    """Logits of probe positions grouped into tool-name spans."""
+    logits: np.ndarray      # [n_rows, vocab] storage dtype
+    span_off: np.ndarray    # [n_probes + 1] int32, span p = rows span_off[p] .. span_off[p+1]-1
+    vocab: int
+    dtype: str
+
+
+def probe_batch(n_probes, vocab, dtype=BF16, span=(0, 12), seed=0, tie_prob=0.05, neg_inf_prob=0.0):
+    """Probe positions of a D2 confidence check (Section 4.2).
+
+    Span lengths are uniform in ``span`` (inclusive; 0 and 1 leave nothing to
+    score). Each row is standard normal logits plus a boost on one random
+    token of ln(vocab) + 0.5 + u, u uniform in [-4, 8], which spreads the
+    top-1 probability from about 0.02 to above 0.999 (around 0.9 near
+    u = 2.2); with probability ``tie_prob`` a second token gets the same boost
+    (a tie), and each entry is -inf with probability ``neg_inf_prob`` (a
+    masked vocabulary entry; the boosted tokens never are). Drawn from
+    ``numpy.random.default_rng([42, 5, seed])``.
+    """
+    rng = np.random.default_rng([42, 5, seed])
+    lens = rng.integers(span[0], span[1] + 1, size=n_probes)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    rows = int(off[-1])
+    x = rng.standard_normal((rows, vocab)).astype(np.float32)
+    if neg_inf_prob > 0:
+        x[rng.random((rows, vocab)) < neg_inf_prob] = -np.inf
+    boost = (math.log(vocab) + 0.5 + rng.uniform(-4.0, 8.0, size=rows)).astype(np.float32)
+    target = rng.integers(0, vocab, size=rows)
+    tie = rng.random(rows) < tie_prob
+    partner = (target + 1 + rng.integers(0, max(vocab - 1, 1), size=rows)) % vocab
+    x[np.arange(rows), target] = boost
+    x[np.arange(rows)[tie], partner[tie]] = boost[tie]
+    return ProbeBatch(logits=to_storage(x, dtype), span_off=off, vocab=vocab, dtype=dtype)

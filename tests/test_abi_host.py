@@ -148,6 +148,33 @@ def test_error_codes():
     spork.spork_cache_destroy(c)
 
 
+def test_confidence_error_codes():
+    """Bad arguments of spork_probe_confidence fail on the host, before any launch."""
+    conf = spork.spork_probe_confidence
+    with pytest.raises(spork.SporkError) as e:
+        conf(256, 7, 100, 4, 256, 1, 0.9, None, None, 256, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_UNSUPPORTED
+    for bad in ((256, 0, -1, 4), (256, 0, 100, -1)):          # vocab, n_rows
+        with pytest.raises(spork.SporkError) as e:
+            conf(bad[0], bad[1], bad[2], bad[3], 256, 1, 0.9, None, None, 256, None, None, stream=0)
+        assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:                 # NULL logits
+        conf(None, 0, 100, 4, 256, 1, 0.9, None, None, 256, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:                 # NULL confidence_out
+        conf(256, 0, 100, 4, 256, 1, 0.9, None, None, None, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:                 # no workspace
+        conf(256, 0, 100, 4, 256, 1, 0.9, None, None, 256, None, None, stream=0)
+    assert e.value.code == spork.SPORK_E_CAPACITY
+    # per (row, chunk) a 64-bit key and a (max, sum) float pair
+    for rows, vocab in ((0, 100), (1, 151936), (40, 151936), (3, 7)):
+        chunks = max(1, min(max(vocab // 8192, 1), (2048 + rows - 1) // rows if rows else 1))
+        assert spork.spork_confidence_workspace_bytes(rows, vocab) == rows * chunks * 16
+    # nothing to do: no launch, success
+    conf(None, 0, 100, 0, None, 0, 0.9, None, None, None, None, None, stream=0)
+
+
 def _plan_for(wl, groups=None, n_cu=256):
     c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
     for stp in wl.steps:
