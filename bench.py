@@ -202,7 +202,7 @@ def main():
         return
 
     t_gen = time.perf_counter()
-    wl = synth.make(args.workload)
+    wl = synth.make_tree() if args.workload == synth.TREE_NAME else synth.make(args.workload)
     print(f"# workload {wl.name}: generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
 
     # Host work of the forks: replay the scenario's block-manager calls alone.
@@ -290,7 +290,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == synth.BF16 else "f32",
-        "data": "synthetic (seeded Gaussian K/V/Q, planted greedy logits)",
+        "data": "synthetic (seeded Gaussian K/V/Q" + (", planted greedy logits)" if logits_bytes else ")"),
         "config": {
             "workload": wl.name, "query_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.d,
             "block_size": wl.block_size, "sessions": len(wl.prefix_len),

@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstring>
+#include <functional>
 #include <map>
 
 namespace spork {
@@ -80,39 +81,65 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   p.n_rows = static_cast<int32_t>(total_rows);
   p.n_groups = static_cast<int32_t>(members.size());
 
+  // Ranges of each fork group: a prefix tree over the members' block tables.
+  // `split(S, b)` takes members S that hold the same blocks [0, b) and whose
+  // rows all see positions [0, b * bs); it sorts them by their block at index
+  // b. A class of one member reads the rest of its context privately. A
+  // larger class shares the longest run of blocks its members agree on,
+  // capped so that every row of every member sees all of it, and then splits
+  // again behind it. Staggered forks (probes forked at different points of
+  // the main thread's chain of thought) give one nested level per fork point.
   std::vector<Range> ranges;
-  for (const auto& m : members) {
-    for (int32_t t : m) p.flat_tokens += len[t];
-    if (m.size() == 1) {
-      const int32_t t = m[0];
-      ranges.push_back({0, len[t], t, {t}});
-      p.private_tokens += len[t];
-      continue;
+  std::vector<const std::vector<int32_t>*> tab(n_threads);
+  for (int32_t t = 0; t < n_threads; ++t) tab[t] = &bm.table(seqs[t]);
+  auto add_private = [&](int32_t t, int32_t lo) {
+    if (len[t] > lo) {
+      ranges.push_back({lo, len[t], t, {t}});
+      p.private_tokens += len[t] - lo;
     }
-    // Longest common prefix of the members' tables, in whole blocks ...
-    size_t lcp = bm.table(seqs[m[0]]).size();
-    for (int32_t t : m) lcp = std::min(lcp, bm.table(seqs[t]).size());
-    const auto& t0 = bm.table(seqs[m[0]]);
-    size_t i = 0;
-    for (; i < lcp; ++i) {
-      bool same = true;
-      for (int32_t t : m) same = same && bm.table(seqs[t])[i] == t0[i];
-      if (!same) break;
-    }
-    // ... capped so that every row of every member sees the whole prefix.
-    int64_t shared = static_cast<int64_t>(i) * bs;
-    for (int32_t t : m) shared = std::min<int64_t>(shared, len[t] - n_rows[t] + 1);
-    const int32_t P = static_cast<int32_t>(shared);
-    if (P > 0) {
-      ranges.push_back({0, P, m[0], m});
-      p.shared_tokens += P;
-    }
-    for (int32_t t : m) {
-      if (len[t] > P) {
-        ranges.push_back({P, len[t], t, {t}});
-        p.private_tokens += len[t] - P;
+  };
+  std::function<void(const std::vector<int32_t>&, size_t)> split = [&](const std::vector<int32_t>& S, size_t b) {
+    const int32_t lo = static_cast<int32_t>(b) * bs;
+    std::vector<std::vector<int32_t>> classes;
+    std::map<int32_t, size_t> by_block;
+    for (int32_t t : S) {
+      if (tab[t]->size() <= b) continue;  // no tokens at or past lo
+      const auto it = by_block.find((*tab[t])[b]);
+      if (it == by_block.end()) {
+        by_block.emplace((*tab[t])[b], classes.size());
+        classes.push_back({t});
+      } else {
+        classes[it->second].push_back(t);
       }
     }
+    for (const auto& C : classes) {
+      if (C.size() == 1) {
+        add_private(C[0], lo);
+        continue;
+      }
+      size_t e = b + 1;
+      for (;; ++e) {
+        bool same = true;
+        for (int32_t t : C) same = same && tab[t]->size() > e && (*tab[t])[e] == (*tab[C[0]])[e];
+        if (!same) break;
+      }
+      int64_t shared = static_cast<int64_t>(e) * bs;
+      for (int32_t t : C) shared = std::min<int64_t>(shared, len[t] - n_rows[t] + 1);
+      const int32_t P = static_cast<int32_t>(shared);
+      if (P > lo) {
+        ranges.push_back({lo, P, C[0], C});
+        p.shared_tokens += P - lo;
+      }
+      if (P >= lo && static_cast<int64_t>(P) == static_cast<int64_t>(e) * bs) {
+        split(C, e);
+      } else {
+        for (int32_t t : C) add_private(t, std::max(P, lo));
+      }
+    }
+  };
+  for (const auto& m : members) {
+    for (int32_t t : m) p.flat_tokens += len[t];
+    split(m, 0);
   }
 
   // Row tiles per workgroup: large row sets are split into near-equal slices

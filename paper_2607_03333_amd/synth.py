@@ -106,6 +106,8 @@ class Thread:
     role: str           # "main" or "probe"
     suffix: int         # private tokens appended after the fork (includes the decode token)
     drafts: int = 0     # draft tokens appended before the verify step
+    parent: int = -1    # sequence forked from (-1: a root that owns its session prefix)
+    fork_len: int = 0   # parent's context length at the fork
 
 
 @dataclass
@@ -145,11 +147,19 @@ class Workload:
     suffix_v: dict
     steps: list = field(default_factory=list)
 
+    def thread(self, seq):
+        return next(t for t in self.threads if t.seq == seq)
+
     def context(self, seq, length=None):
-        """Logical K, V of a thread (prefix then private tokens), storage dtype."""
-        t = next(t for t in self.threads if t.seq == seq)
-        k = np.concatenate([self.prefix_k[t.session], self.suffix_k[seq]])
-        v = np.concatenate([self.prefix_v[t.session], self.suffix_v[seq]])
+        """Logical K, V of a thread, storage dtype: a root's session prefix, or
+        its parent's context up to the fork, then its own tokens."""
+        t = self.thread(seq)
+        if t.parent >= 0:
+            pk, pv = self.context(t.parent, t.fork_len)
+        else:
+            pk, pv = self.prefix_k[t.session], self.prefix_v[t.session]
+        k = np.concatenate([pk, self.suffix_k[seq]])
+        v = np.concatenate([pv, self.suffix_v[seq]])
         if length is not None:
             k, v = k[:length], v[:length]
         return k, v
@@ -176,15 +186,27 @@ class Workload:
         return n
 
     def unique_kv_bytes(self, step_index):
-        """KV bytes a step must read once: each shared prefix once, each private part once."""
+        """KV bytes a step must read once: every stored token that one of the
+        step's threads sees, once. A forked thread shares its parent's blocks
+        up to the block holding the fork point; from that block on its tokens
+        are its own copy (the block is copied on the first write)."""
         step = self.steps[step_index]
         elem = 4 if self.dtype == F32 else 2
         per_tok = 2 * self.hkv * self.d * elem
-        sessions = sorted({next(t.session for t in self.threads if t.seq == s) for s in step.seqs})
-        total = sum(self.prefix_len[s] for s in sessions)
+        bs = self.block_size
+
+        def own_lo(t):
+            return 0 if t.parent < 0 else (t.fork_len // bs) * bs
+
+        upper = {}
         for s in step.seqs:
-            t = next(t for t in self.threads if t.seq == s)
-            total += self.thread_len(s, step_index) - self.prefix_len[t.session]
+            t, hi = self.thread(s), self.thread_len(s, step_index)
+            while True:
+                upper[t.seq] = max(upper.get(t.seq, 0), hi)
+                if t.parent < 0:
+                    break
+                hi, t = own_lo(t), self.thread(t.parent)
+        total = sum(max(0, hi - own_lo(self.thread(q))) for q, hi in upper.items())
         return total * per_tok
 
 
@@ -240,7 +262,7 @@ def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=No
     nid = n_sess
     for s in range(n_sess):
         for _ in range(n_probe):
-            threads.append(Thread(seq=nid, session=s, role="probe", suffix=0))
+            threads.append(Thread(seq=nid, session=s, role="probe", suffix=0, parent=s, fork_len=plen))
             nid += 1
     by_session = {s: [t for t in threads if t.session == s] for s in range(n_sess)}
     ordered = [t for s in range(n_sess) for t in by_session[s]]   # main, probes per session
@@ -385,3 +407,91 @@ def probe_batch(n_probes, vocab, dtype=BF16, span=(0, 12), seed=0, tie_prob=0.05
     x[np.arange(rows), target] = boost
     x[np.arange(rows)[tie], partner[tie]] = boost[tie]
     return ProbeBatch(logits=to_storage(x, dtype), span_off=off, vocab=vocab, dtype=dtype)
+
+
+TREE_NAME = "qwen3-30b-a3b-staggered"
+
+
+def make_tree(sessions=32, prefix=32768, probes=4, stride=200, probe_tokens=(8, 64), main_extra=(1, 200),
+              hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0):
+    """Staggered probes (Algorithm 1's retry loop): a decode step over a
+    prefix tree of forks.
+
+    Per session the main thread holds the ``prefix``-token prompt; after its
+    first CoT token it forks probe 0, and after every further ``stride`` CoT
+    tokens the next probe (Algorithm 1 forks probe r once the main thread has
+    decoded r * s more tokens; the paper does not give s, and 200 puts the
+    fork points in the middle of 16-token blocks). The main thread then
+    decodes ``main_extra`` (uniform, inclusive) more tokens and every probe
+    holds ``probe_tokens`` (uniform) of its own: the forced tool-call opener
+    and the tool call decoded so far. Probe r therefore shares
+    ``prefix + 1 + r * stride`` tokens with the main thread and with every
+    later probe. The step decodes one row for every thread, the threads of a
+    session forming one fork group. Default shapes are the Qwen3-30B-A3B
+    attention (32 query heads, 4 KV heads, head dim 128, bf16). Seeds:
+    ``default_rng([42, 6])`` for lengths, order and Q; K and V of the prefix
+    and of each thread's own tokens from ``[42, 6, 1, s]`` and ``[42, 6, 2, seq]``.
+    """
+    index = 6
+    rng = np.random.default_rng([42, index])
+    bs = block_size
+    threads = [Thread(seq=s, session=s, role="main", suffix=0) for s in range(sessions)]
+    nid = sessions
+    for s in range(sessions):
+        for r in range(probes):
+            threads.append(Thread(seq=nid, session=s, role="probe", suffix=0, parent=s,
+                                  fork_len=prefix + 1 + r * stride))
+            nid += 1
+    by_session = {s: [t for t in threads if t.session == s] for s in range(sessions)}
+    ordered = [t for s in range(sessions) for t in by_session[s]]
+    extra = rng.integers(main_extra[0], main_extra[1] + 1, size=sessions)
+    for s in range(sessions):
+        by_session[s][0].suffix = 1 + max(probes - 1, 0) * stride + int(extra[s])
+    own = rng.integers(probe_tokens[0], probe_tokens[1] + 1, size=sessions * probes)
+    for t, n in zip([t for t in ordered if t.role == "probe"], own):
+        t.suffix = int(n)
+
+    blocks = sessions * -(-prefix // bs) + sum(-(-t.suffix // bs) + 2 for t in threads)
+    num_blocks = blocks + 16
+    free_order = rng.permutation(num_blocks).astype(np.int32)
+
+    def normal(shape, r=rng):
+        return r.standard_normal(shape, dtype=np.float32)
+
+    def kv_pair(key, n):
+        r = np.random.default_rng([42, index] + list(key))
+        return (to_storage(normal((n, hkv, d), r), dtype),
+                to_storage(normal((n, hkv, d), r), dtype))
+
+    jobs = [((1, s), prefix) for s in range(sessions)] + [((2, t.seq), t.suffix) for t in ordered]
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
+    suffix_k = {t.seq: pairs[sessions + i][0] for i, t in enumerate(ordered)}
+    suffix_v = {t.seq: pairs[sessions + i][1] for i, t in enumerate(ordered)}
+
+    ops = []
+    for s in range(sessions):
+        main = by_session[s][0]
+        ops += [("new", main.seq), ("append", main.seq, prefix)]
+    for s in range(sessions):
+        main = by_session[s][0]
+        done = 0
+        for t in by_session[s][1:]:
+            step = t.fork_len - prefix - done
+            ops.append(("append", main.seq, step))
+            done += step
+            ops.append(("fork", main.seq, t.seq))
+        ops.append(("append", main.seq, main.suffix - done))
+    for t in ordered:
+        if t.role == "probe":
+            ops.append(("append", t.seq, t.suffix))
+
+    wl = Workload(index=index, name=TREE_NAME, hq=hq, hkv=hkv, d=d, block_size=bs, dtype=dtype,
+                  logits_dtype=dtype, sm_scale=float(np.float32(1.0 / math.sqrt(d))),
+                  num_blocks=num_blocks, free_order=free_order, threads=threads,
+                  prefix_len=[prefix] * sessions, prefix_k=[pairs[s][0] for s in range(sessions)],
+                  prefix_v=[pairs[s][1] for s in range(sessions)], suffix_k=suffix_k, suffix_v=suffix_v)
+    q = to_storage(normal((len(ordered), hq, d)) * np.float32(q_gain), dtype)
+    wl.steps.append(Step(seqs=[t.seq for t in ordered], n_rows=[1] * len(ordered),
+                         groups=[t.session for t in ordered], q=q, ops_before=ops))
+    return wl

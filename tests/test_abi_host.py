@@ -214,11 +214,10 @@ def test_plan_unique_bytes_match_workload(index):
     spork.spork_cache_destroy(c)
 
 
-def test_plan_covers_every_output_once_per_token():
+def _check_cover(wl, c, p):
     """Decode the image: for every output (query row, head), the workgroups
-    that write one of its partials cover each visible position exactly once."""
-    wl = synth.make(4, sessions=3, prefix=200, suffix=("uniform", 1, 90))
-    c, p = _plan_for(wl, n_cu=4)
+    that write one of its partials cover each visible position exactly once,
+    through block-table entries equal to the thread's own table."""
     info, img = _decode_image(p)
     raw = img.view(np.int32)
     # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, merge_ids
@@ -229,7 +228,12 @@ def test_plan_covers_every_output_once_per_token():
     off += -(-info["n_items"] * 24 // 256) * 256 // 4
     nrow_desc = int(items[:, 4].sum())
     rows = raw[off: off + 2 * nrow_desc].reshape(-1, 2)
+    off += -(-nrow_desc * 8 // 256) * 256 // 4
+    tables = raw[off:]
     stp = wl.steps[-1]
+    row_seq = [s for s, n in zip(stp.seqs, stp.n_rows) for _ in range(n)]
+    own = {s: spork.spork_block_table(c, s) for s in stp.seqs}
+    bs = wl.block_size
     cover = {}
     for w in waves:
         item, lo, hi, row0, nr, part = (int(x) for x in w)
@@ -238,12 +242,16 @@ def test_plan_covers_every_output_once_per_token():
         it = items[item]
         for i in range(nr):
             qidx, hz = rows[it[3] + row0 + i]
-            cover.setdefault(int(qidx), []).append((lo, min(hi, hz + 1)))
+            top = min(hi, int(hz) + 1)
+            cover.setdefault(int(qidx), []).append((lo, top))
+            if top > lo:
+                seq = row_seq[int(qidx) // wl.hq]
+                blk = np.arange(lo // bs, (top - 1) // bs + 1)
+                assert np.all(blk < it[2])
+                assert np.array_equal(tables[it[1] + blk], own[seq][blk]), (seq, lo, top)
     assert len(cover) == sum(stp.n_rows) * wl.hq
     row = 0
-    lens = {s: 0 for s in stp.seqs}
-    for s in stp.seqs:
-        lens[s] = spork.spork_seq_len(c, s)
+    lens = {s: spork.spork_seq_len(c, s) for s in stp.seqs}
     for s, n in zip(stp.seqs, stp.n_rows):
         for r in range(n):
             for h in range(wl.hq):
@@ -253,6 +261,54 @@ def test_plan_covers_every_output_once_per_token():
                     seen[lo:hi] += 1
                 assert seen[: pos + 1].min() == 1 and seen[: pos + 1].max() == 1
         row += n
+
+
+def test_plan_covers_every_output_once_per_token():
+    wl = synth.make(4, sessions=3, prefix=200, suffix=("uniform", 1, 90))
+    c, p = _plan_for(wl, n_cu=4)
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+@pytest.mark.parametrize("prefix,stride,probes", [(256, 40, 4), (1000, 37, 3), (64, 16, 5), (300, 200, 2)])
+def test_staggered_tree_plan(prefix, stride, probes):
+    """Probes forked at staggered points share nested prefixes: one shared
+    range per fork point, ending at the block that holds the fork point (that
+    block is copied on the first write), and every output still sees each
+    position once through its own blocks."""
+    wl = synth.make_tree(sessions=3, prefix=prefix, stride=stride, probes=probes, probe_tokens=(1, 20),
+                         main_extra=(1, 40), hq=4, hkv=2, d=64, dtype=synth.F32)
+    c, p = _plan_for(wl, n_cu=8)
+    info = spork.spork_plan_get_info(p)
+    bs = wl.block_size
+    forks = [prefix + 1 + r * stride for r in range(probes)]
+    # first level: the prompt's whole blocks, then one level per later fork point
+    want_shared = 3 * (forks[-1] // bs * bs)
+    assert info["shared_tokens"] == want_shared
+    assert info["unique_kv_bytes"] == wl.unique_kv_bytes(0)
+    assert info["unique_kv_bytes"] < info["flat_kv_bytes"]
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+def test_tree_plan_degenerate_groups():
+    """Probes forked at the same point, a probe never written after its fork,
+    and a group whose members share nothing."""
+    wl = synth.make_tree(sessions=2, prefix=96, stride=0, probes=3, probe_tokens=(0, 0), main_extra=(1, 9),
+                         hq=4, hkv=2, d=64, dtype=synth.F32)
+    c, p = _plan_for(wl, n_cu=4)
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+    # every thread in one group across sessions: sessions share no block
+    wl = synth.make_tree(sessions=2, prefix=64, stride=20, probes=2, probe_tokens=(1, 5), main_extra=(1, 9),
+                         hq=4, hkv=2, d=64, dtype=synth.F32)
+    c, p = _plan_for(wl, groups=[0] * len(wl.steps[0].seqs), n_cu=4)
+    info = spork.spork_plan_get_info(p)
+    assert info["unique_kv_bytes"] == wl.unique_kv_bytes(0)
+    _check_cover(wl, c, p)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)
 

@@ -110,3 +110,17 @@ def test_accept_only_mode_and_all_or_nothing_drafts():
     assert np.array_equal(step.accept_len.cpu().numpy(), st.planted_accept)
     assert np.array_equal(step.next_token.cpu().numpy(), st.planted_next)
     dw.close()
+
+
+@pytest.mark.parametrize("prefix,stride,probes,dtype,shape", [
+    (1000, 37, 4, synth.F32, dict(hq=4, hkv=2, d=64)),      # unaligned prompt, fork points mid-block
+    (4096, 200, 4, synth.BF16, dict()),                      # Qwen3-30B-A3B attention shapes
+    (256, 16, 6, synth.BF16, dict(hq=64, hkv=8)),            # one fork per block, deep tree
+    (640, 0, 3, synth.BF16, dict()),                         # probes forked at the same point
+])
+def test_staggered_fork_tree(prefix, stride, probes, dtype, shape):
+    say(f"staggered tree prefix={prefix} stride={stride} probes={probes} {dtype} {shape}")
+    wl = synth.make_tree(sessions=3, prefix=prefix, stride=stride, probes=probes, probe_tokens=(1, 40),
+                         main_extra=(1, 60), dtype=dtype, **shape)
+    dw = run_workload(wl, f"tree p{prefix} s{stride} r{probes}")
+    dw.close()
