@@ -162,6 +162,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--verify-k", type=int, default=0,
+                    help="draft length of the verify workloads (default: the workload's own)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -202,7 +204,7 @@ def main():
         return
 
     t_gen = time.perf_counter()
-    wl = synth.make_tree() if args.workload == synth.TREE_NAME else synth.make(args.workload)
+    wl = synth.make_named(args.workload, **({"verify_k": args.verify_k} if args.verify_k else {}))
     print(f"# workload {wl.name}: generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
 
     # Host work of the forks: replay the scenario's block-manager calls alone.

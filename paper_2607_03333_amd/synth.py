@@ -495,3 +495,88 @@ def make_tree(sessions=32, prefix=32768, probes=4, stride=200, probe_tokens=(8, 
     wl.steps.append(Step(seqs=[t.seq for t in ordered], n_rows=[1] * len(ordered),
                          groups=[t.session for t in ordered], q=q, ops_before=ops))
     return wl
+
+
+PREFILL_NAME = "qwen3-30b-a3b-probe-prefill"
+
+
+def make_prefill(sessions=64, prefix=32768, probes=2, cot=("loguniform", 1, 4096), opener=(8, 50),
+                 hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0):
+    """Probe prefill over the shared prefix (Section 4.1: the probe's prefill
+    is a prefix-cache hit): one step in which every main thread decodes one
+    row while its probes, just forked after the chain of thought observed so
+    far, prefill their forced tool-call openers as multi-row causal queries.
+
+    Per session the main thread holds a ``prefix``-token prompt and ``cot``
+    tokens of chain of thought (log-uniform, as the bench workload's private
+    suffixes); ``probes`` probes fork there; each probe then appends its
+    opener of ``opener`` tokens (uniform, inclusive) and queries all of them,
+    causally among themselves, while the main thread appends and queries its
+    next token. Default shapes are the Qwen3-30B-A3B attention. Seeds:
+    ``default_rng([42, 7])`` for lengths, order and Q; K and V from
+    ``[42, 7, 1, session]`` and ``[42, 7, 2, seq]``.
+    """
+    index = 7
+    rng = np.random.default_rng([42, index])
+    bs = block_size
+    cot_len = _draw_suffix(rng, cot, sessions)
+    threads = [Thread(seq=s, session=s, role="main", suffix=cot_len[s] + 1) for s in range(sessions)]
+    nid = sessions
+    for s in range(sessions):
+        for _ in range(probes):
+            threads.append(Thread(seq=nid, session=s, role="probe", suffix=0, parent=s,
+                                  fork_len=prefix + cot_len[s]))
+            nid += 1
+    by_session = {s: [t for t in threads if t.session == s] for s in range(sessions)}
+    ordered = [t for s in range(sessions) for t in by_session[s]]
+    op_len = rng.integers(opener[0], opener[1] + 1, size=sessions * probes)
+    for t, n in zip([t for t in ordered if t.role == "probe"], op_len):
+        t.suffix = int(n)
+
+    blocks = sessions * -(-prefix // bs) + sum(-(-t.suffix // bs) + 2 for t in threads)
+    num_blocks = blocks + 16
+    free_order = rng.permutation(num_blocks).astype(np.int32)
+
+    def normal(shape, r=rng):
+        return r.standard_normal(shape, dtype=np.float32)
+
+    def kv_pair(key, n):
+        r = np.random.default_rng([42, index] + list(key))
+        return (to_storage(normal((n, hkv, d), r), dtype),
+                to_storage(normal((n, hkv, d), r), dtype))
+
+    jobs = [((1, s), prefix) for s in range(sessions)] + [((2, t.seq), t.suffix) for t in ordered]
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
+    suffix_k = {t.seq: pairs[sessions + i][0] for i, t in enumerate(ordered)}
+    suffix_v = {t.seq: pairs[sessions + i][1] for i, t in enumerate(ordered)}
+
+    ops = []
+    for s in range(sessions):
+        ops += [("new", s), ("append", s, prefix + cot_len[s])]
+    for t in ordered:
+        if t.role == "probe":
+            ops.append(("fork", t.parent, t.seq))
+    for t in ordered:
+        ops.append(("append", t.seq, 1 if t.role == "main" else t.suffix))
+
+    wl = Workload(index=index, name=PREFILL_NAME, hq=hq, hkv=hkv, d=d, block_size=bs, dtype=dtype,
+                  logits_dtype=dtype, sm_scale=float(np.float32(1.0 / math.sqrt(d))),
+                  num_blocks=num_blocks, free_order=free_order, threads=threads,
+                  prefix_len=[prefix] * sessions, prefix_k=[pairs[s][0] for s in range(sessions)],
+                  prefix_v=[pairs[s][1] for s in range(sessions)], suffix_k=suffix_k, suffix_v=suffix_v)
+    rows = [1 if t.role == "main" else t.suffix for t in ordered]
+    q = to_storage(normal((sum(rows), hq, d)) * np.float32(q_gain), dtype)
+    wl.steps.append(Step(seqs=[t.seq for t in ordered], n_rows=rows, groups=[t.session for t in ordered],
+                         q=q, ops_before=ops))
+    return wl
+
+
+def make_named(name, **kw):
+    """Any workload by name: the five benchmark workloads, the staggered fork
+    tree and the probe prefill."""
+    if name == TREE_NAME:
+        return make_tree(**kw)
+    if name == PREFILL_NAME:
+        return make_prefill(**kw)
+    return make(name, **kw)

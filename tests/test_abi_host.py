@@ -380,3 +380,19 @@ def test_plan_lists(index, n_cu, shrink):
     assert loads.max() <= share + max(2 * (512 + 256), longest_small), (loads.max(), share)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)
+
+
+@pytest.mark.parametrize("shape", [dict(hq=4, hkv=2, d=64, dtype=synth.F32), dict()])
+def test_probe_prefill_plan(shape):
+    """Multi-row probes forked after the chain of thought: the prefix up to the
+    block holding the fork point is shared by the main row and every opener
+    row, each row sees each position up to its own once."""
+    wl = synth.make_prefill(sessions=3, prefix=300, cot=("uniform", 1, 100), opener=(8, 50), **shape)
+    c, p = _plan_for(wl, n_cu=8)
+    info = spork.spork_plan_get_info(p)
+    assert info["unique_kv_bytes"] == wl.unique_kv_bytes(0)
+    forks = [t.fork_len for t in wl.threads if t.role == "probe"][::2]
+    assert info["shared_tokens"] == sum(f // wl.block_size * wl.block_size for f in forks)
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)

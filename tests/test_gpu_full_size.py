@@ -3,8 +3,8 @@
 The whole batch runs through the C ABI; the oracle recomputes a sample of
 threads one by one (the first and last thread, the longest context, the
 shortest private range, a verify thread where there is one, and for the
-staggered fork tree every thread of the first and last session), element by
-element. Argmax and accept are compared on every row, bit-exactly, against
+staggered fork tree and the probe prefill every thread of the first and last
+session), element by element. Argmax and accept are compared on every row, bit-exactly, against
 the oracle and against the generator's planted values. Every output is also
 checked by a second run: which workgroup computes which chunk of a unit
 changes from run to run, so a chunk lost or counted twice anywhere in the
@@ -30,16 +30,18 @@ def _pick(wl, step_index):
     verify = [i for i, r in enumerate(st.n_rows) if r > 1]
     if verify:
         pick.add(verify[-1])
-    if wl.name == synth.TREE_NAME:
+    if wl.name in (synth.TREE_NAME, synth.PREFILL_NAME):
         # every thread of the first and the last session: each level of both trees
         sess = [wl.thread(q).session for q in st.seqs]
         pick |= {i for i, x in enumerate(sess) if x in (sess[0], sess[-1])}
     return sorted(pick)
 
 
-@pytest.mark.parametrize("index", [0, 1, 2, 3, 4, synth.TREE_NAME])
-def test_full_size_workload(index):
-    wl = synth.make_tree() if index == synth.TREE_NAME else synth.make(index)
+@pytest.mark.parametrize("index,over", [(0, {}), (1, {}), (2, {}), (3, {}), (4, {}), (synth.TREE_NAME, {}),
+                                        (synth.PREFILL_NAME, {}), ("qwen3-32b-verify", dict(verify_k=50))],
+                         ids=["0", "1", "2", "3", "4", "tree", "prefill", "verify-k50"])
+def test_full_size_workload(index, over):
+    wl = synth.make_named(index, **over)
     say(f"[full {wl.name}] generated; blocks {wl.num_blocks}")
     dw = runner.DeviceWorkload(wl, poison_pool=True)
     try:

@@ -124,3 +124,26 @@ def test_staggered_fork_tree(prefix, stride, probes, dtype, shape):
                          main_extra=(1, 60), dtype=dtype, **shape)
     dw = run_workload(wl, f"tree p{prefix} s{stride} r{probes}")
     dw.close()
+
+
+@pytest.mark.parametrize("dtype,shape,opener", [
+    (synth.BF16, dict(), (8, 50)),                     # Qwen3-30B-A3B shapes: 64-400 rows per KV head
+    (synth.F32, dict(hq=4, hkv=2, d=64), (1, 23)),    # ragged row tiles in fp32
+    (synth.BF16, dict(hq=64, hkv=8), (40, 50)),        # 320-400 rows per KV head: several row slices
+])
+def test_probe_prefill(dtype, shape, opener):
+    """Probes prefill their forced openers (multi-row causal queries) over the
+    prefix they share with the main thread, which decodes one row."""
+    say(f"probe prefill {dtype} {shape} opener {opener}")
+    wl = synth.make_prefill(sessions=3, prefix=700, cot=("uniform", 1, 300), opener=opener, dtype=dtype, **shape)
+    dw = run_workload(wl, f"prefill {dtype} {opener}")
+    dw.close()
+
+
+def test_verify_k50():
+    """Verify at the paper's draft length (K = 50): 51 causal rows per
+    session, accept lengths planted up to K."""
+    say("verify K=50")
+    wl = synth.make(3, sessions=3, prefix=600, verify_k=50, vocab=2000)
+    dw = run_workload(wl, "verify k50")
+    dw.close()
