@@ -17,6 +17,9 @@ paper it follows (SPORK, arXiv 2607.03333):
   matches them (Section 4.3, steps 2-3; Appendix B).
 * confidence: the top-1 log-probability of each probe position and the D2
   gate over the tool-name span (Section 4.2).
+* ngram: the prompt-lookup draft proposer of the engine's n-gram speculative
+  decoding, the drafts' second source beside the probe body (Sections 4.3,
+  6.1).
 
 Parity status of each function is stated in its module header.
 """
@@ -26,9 +29,11 @@ from .kv import scatter_tokens, gather_context
 from .attention import attend, attend_batch
 from .accept import argmax_rows, accept_drafts
 from .confidence import top1_logprob, span_confidence, confidence_gate
+from .ngram import ngram_propose, ngram_propose_one
 
 __all__ = [
     "BlockManager", "NoBlocksError", "scatter_tokens", "gather_context",
     "attend", "attend_batch", "argmax_rows", "accept_drafts",
     "top1_logprob", "span_confidence", "confidence_gate",
+    "ngram_propose", "ngram_propose_one",
 ]
