@@ -156,6 +156,56 @@ def confidence_bench(args, torch, spork, synth):
                      "avg_launch_ms": round(ms_chunks, 4), "algorithmic_bytes_per_launch": nbytes}}), flush=True)
 
 
+def ngram_bench(args, torch, spork, synth):
+    """n-gram draft proposer alone: one JSON line, HBM roofline of the scan
+    (4 bytes per token read once)."""
+    import numpy as np
+    n = args.ngram_seqs
+    tok, off = synth.token_histories(n, (32768, 36864), seed=1)
+    dev = torch.device("cuda:0")
+    t = torch.from_numpy(tok).to(dev)
+    o = torch.from_numpy(off).to(dev)
+    k, n_min, n_max = 8, 2, 4
+    max_len = int(np.diff(off).max())
+    drafts = torch.empty(n * k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = torch.empty(spork.spork_ngram_workspace_bytes(n, max_len), dtype=torch.uint8, device=dev)
+
+    def step():
+        spork.spork_ngram_propose(t, o, n, max_len, n_min, n_max, k, drafts, cnt, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spork.spork_timing_read()
+    spork.spork_timing_enable(True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    spork.spork_timing_enable(False)
+    kern = spork.spork_timing_read()
+    ms_step = start.elapsed_time(end) / args.steps
+    nbytes = int(tok.size) * 4
+    ms_scan = kern["ngram_scan"][0] / max(kern["ngram_scan"][1], 1)
+    achieved = nbytes / (ms_scan * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "n-gram draft proposer: token GB/s", "value": round(nbytes / (ms_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32", "data": "synthetic (segments copied from earlier in the sequence or Zipf tokens)",
+        "config": {"workload": "ngram-histories", "sequences": n, "tokens": int(tok.size), "n_min": n_min,
+                   "n_max": n_max, "k": k},
+        "kernel_ms_per_step": {kk: round(v[0] / max(v[1], 1), 4) for kk, v in kern.items() if v[1]},
+        "with_drafts": int((cnt > 0).sum().item()),
+        "roofline": {"bound": "hbm", "kernel": "ngram_scan", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_launch_ms": round(ms_scan, 4), "algorithmic_bytes_per_launch": nbytes}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,6 +222,9 @@ def main():
     ap.add_argument("--confidence-probes", type=int, default=0,
                     help="instead of the benchmark, time the D2 confidence gate over this many probe "
                          "spans (0..16 positions each) of the 151,936-token vocabulary, bf16 logits")
+    ap.add_argument("--ngram-seqs", type=int, default=0,
+                    help="instead of the benchmark, time the n-gram draft proposer over this many "
+                         "token histories of 32768-36864 tokens")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -201,6 +254,9 @@ def main():
 
     if args.confidence_probes:
         confidence_bench(args, torch, spork, synth)
+        return
+    if args.ngram_seqs:
+        ngram_bench(args, torch, spork, synth)
         return
 
     t_gen = time.perf_counter()

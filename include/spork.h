@@ -20,6 +20,9 @@
  *     log-probability of every probe position and, per probe, the smallest
  *     top-1 probability over its tool-name span without the span's first
  *     token, compared with a threshold.
+ *   - spork_ngram_propose: the n-gram (prompt-lookup) draft proposer of the
+ *     engine's n-gram speculative decoding (Sections 4.3 and 6.1), a second
+ *     source of the drafts spork_verify_accept checks.
  *
  * Conventions
  *   - Every entry point returns SPORK_OK (0) or a negative status and never
@@ -220,7 +223,8 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
  * = first r < k_drafts whose greedy token differs from the draft, else
  * k_drafts; next_token[n_verify] = greedy token of row accept_len;
  * argmax_out[n_verify*(k_drafts+1)] (nullable) = every row's greedy token.
- * Ties pick the lowest vocabulary index; logits must be finite.
+ * Ties pick the lowest vocabulary index; logits must be finite. A draft of
+ * -1 (padding after fewer than k_drafts real drafts) never matches.
  * workspace: the attention's workspace followed (at a 256-byte aligned
  * offset) by spork_verify_workspace_bytes; ws_bytes covers both.
  * With a plan the step is three launches on `stream`: argmax (which also
@@ -262,6 +266,37 @@ int spork_probe_confidence(const void* logits, int32_t logits_dtype, int32_t voc
                            float* confidence_out, int32_t* commit_out, void* workspace,
                            size_t ws_bytes, hipStream_t stream);
 
+/* Workspace for spork_ngram_propose. */
+int spork_ngram_workspace_bytes(int32_t n_seqs, int64_t max_len, size_t* bytes);
+
+/* n-gram (prompt-lookup) drafts for a batch of token sequences: the baseline
+ * draft source of the paper's engine configuration (Section 6.1), which D3's
+ * proposer wraps (Section 4.3).
+ * tokens (device int32): the sequences (prompt and output so far) one after
+ * another; seq_off (device int64 [n_seqs+1]): sequence s is tokens
+ * seq_off[s] .. seq_off[s+1]-1 (offsets non-decreasing, within the tokens
+ * buffer, each sequence shorter than 2^31 tokens; they are read on the
+ * device and not checked).
+ * For each sequence of L tokens: for n from n_max down to n_min, the key is
+ * its last n tokens; the first n whose key occurs earlier, starting at j
+ * with j + n <= L - 1 (occurrences may overlap the key), wins, and of its
+ * occurrences the latest. The drafts are the up to k tokens after that
+ * occurrence, cut at the end of the sequence.
+ * Outputs (device int32): drafts[n_seqs][k], -1 past n_drafts[s] (a value
+ * no greedy token takes, so spork_verify_accept accepts at most the real
+ * drafts); n_drafts[n_seqs] in [0, k].
+ * max_len sizes the launch (one workgroup per 2048 positions of the longest
+ * sequence expected); longer sequences are still scanned whole, more slowly.
+ * workspace (device, 256-byte aligned, ws_bytes >= the size from
+ * spork_ngram_workspace_bytes; any contents on entry).
+ * Two launches on `stream`. SPORK_E_INVAL for bad sizes (1 <= n_min <=
+ * n_max <= 32, 0 <= k <= 4096, 0 <= max_len < 2^31) or a NULL required
+ * pointer, SPORK_E_CAPACITY for a short workspace. */
+int spork_ngram_propose(const int32_t* tokens, const int64_t* seq_off, int32_t n_seqs,
+                        int64_t max_len, int32_t n_min, int32_t n_max, int32_t k,
+                        int32_t* drafts, int32_t* n_drafts, void* workspace, size_t ws_bytes,
+                        hipStream_t stream);
+
 /* ======================================================================== *
  *  Kernel timing (benchmarks).
  * ======================================================================== */
@@ -271,7 +306,9 @@ int spork_probe_confidence(const void* logits, int32_t logits_dtype, int32_t voc
 #define SPORK_KERNEL_ACCEPT 3 /* accept of an accept-only call (plan == NULL) */
 #define SPORK_KERNEL_CONF_CHUNKS 4 /* confidence: per-chunk argmax and sum of exponentials */
 #define SPORK_KERNEL_CONF_FINAL 5  /* confidence: per-row log-probability and per-probe gate */
-#define SPORK_KERNEL_KINDS 6
+#define SPORK_KERNEL_NGRAM_SCAN 6  /* n-gram drafts: per-chunk longest latest key match */
+#define SPORK_KERNEL_NGRAM_DRAFTS 7 /* n-gram drafts: per-sequence choice and draft copy */
+#define SPORK_KERNEL_KINDS 8
 
 /* While enabled (per calling thread), every hot-path call records a HIP event
  * before and after each of its kernels on the caller's stream. */

@@ -2,6 +2,7 @@
 // reporting, block-manager and planner calls, kernel dispatch.
 #include "spork.h"
 
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <exception>
@@ -11,6 +12,7 @@
 
 #include "block_manager.h"
 #include "kernels.h"
+#include "ngram_kernels.h"
 #include "vocab_kernels.h"
 #include "plan.h"
 
@@ -493,6 +495,51 @@ int spork_probe_confidence(const void* logits, int32_t logits_dtype, int32_t voc
     if (rc != SPORK_OK) return rc;
     return hip_status(timed(SPORK_KERNEL_CONF_FINAL, stream, [&] { return spork::launch_conf_final(a, stream); }),
                       "spork_probe_confidence (final)");
+  });
+}
+
+int spork_ngram_workspace_bytes(int32_t n_seqs, int64_t max_len, size_t* bytes) {
+  if (bytes == nullptr) return fail(SPORK_E_INVAL, "bytes is NULL");
+  if (n_seqs < 0 || max_len < 0 || max_len > INT32_MAX)
+    return fail(SPORK_E_INVAL, "n_seqs >= 0 and 0 <= max_len < 2^31 required");
+  *bytes = static_cast<size_t>(n_seqs) * spork::ngram_chunks(max_len) * sizeof(uint64_t);
+  return SPORK_OK;
+}
+
+int spork_ngram_propose(const int32_t* tokens, const int64_t* seq_off, int32_t n_seqs, int64_t max_len,
+                        int32_t n_min, int32_t n_max, int32_t k, int32_t* drafts, int32_t* n_drafts,
+                        void* workspace, size_t ws_bytes, hipStream_t stream) {
+  return guarded([&] {
+    if (n_seqs < 0 || max_len < 0 || max_len > INT32_MAX)
+      return fail(SPORK_E_INVAL, "n_seqs >= 0 and 0 <= max_len < 2^31 required");
+    if (n_min < 1 || n_max < n_min || n_max > spork::kNgramMaxN || k < 0 || k > 4096)
+      return fail(SPORK_E_INVAL, "1 <= n_min <= n_max <= 32 and 0 <= k <= 4096 required");
+    if (n_seqs > 0 && (tokens == nullptr || seq_off == nullptr || n_drafts == nullptr || (k > 0 && drafts == nullptr)))
+      return fail(SPORK_E_INVAL, "NULL pointer");
+    size_t need = 0;
+    spork_ngram_workspace_bytes(n_seqs, max_len, &need);
+    if (ws_bytes < need) return fail(SPORK_E_CAPACITY, "workspace too small");
+    if (need > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
+      return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
+    if (static_cast<int64_t>(n_seqs) * spork::ngram_chunks(max_len) > INT32_MAX)
+      return fail(SPORK_E_INVAL, "batch too large");
+    spork::NgramArgs a{};
+    a.tokens = tokens;
+    a.seq_off = seq_off;
+    a.n_seqs = n_seqs;
+    a.n_chunks = spork::ngram_chunks(max_len);
+    a.n_min = n_min;
+    a.n_max = n_max;
+    a.k = k;
+    a.keys = static_cast<uint64_t*>(workspace);
+    a.drafts = drafts;
+    a.n_drafts = n_drafts;
+    const int rc = hip_status(
+        timed(SPORK_KERNEL_NGRAM_SCAN, stream, [&] { return spork::launch_ngram_scan(a, stream); }),
+        "spork_ngram_propose (scan)");
+    if (rc != SPORK_OK) return rc;
+    return hip_status(timed(SPORK_KERNEL_NGRAM_DRAFTS, stream, [&] { return spork::launch_ngram_drafts(a, stream); }),
+                      "spork_ngram_propose (drafts)");
   });
 }
 

@@ -29,8 +29,11 @@ SPORK_KERNEL_ARGMAX = 2
 SPORK_KERNEL_ACCEPT = 3
 SPORK_KERNEL_CONF_CHUNKS = 4
 SPORK_KERNEL_CONF_FINAL = 5
-SPORK_KERNEL_KINDS = 6
-KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept", "conf_chunks", "conf_final")
+SPORK_KERNEL_NGRAM_SCAN = 6
+SPORK_KERNEL_NGRAM_DRAFTS = 7
+SPORK_KERNEL_KINDS = 8
+KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept", "conf_chunks", "conf_final", "ngram_scan",
+                "ngram_drafts")
 
 _c_i32 = ctypes.c_int32
 _c_i64 = ctypes.c_int64
@@ -91,6 +94,9 @@ _SIGNATURES = {
                                                         ctypes.POINTER(ctypes.c_size_t)]),
     "spork_probe_confidence": (ctypes.c_int, [_p, _c_i32, _c_i32, _c_i32, _p, _c_i32, ctypes.c_float,
                                               _p, _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "spork_ngram_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "spork_ngram_propose": (ctypes.c_int, [_p, _p, _c_i32, _c_i64, _c_i32, _c_i32, _c_i32, _p, _p, _p,
+                                           ctypes.c_size_t, _p]),
     "spork_timing_enable": (ctypes.c_int, [_c_i32]),
     "spork_timing_read": (ctypes.c_int, [_p, _p]),
 }
@@ -300,6 +306,20 @@ def spork_probe_confidence(logits, logits_dtype, vocab, n_rows, span_off, n_prob
                                         n_probes, float(theta), _ptr(argmax_out), _ptr(logprob_out),
                                         _ptr(confidence_out), _ptr(commit_out), _ptr(workspace),
                                         ws_bytes, _stream(stream)))
+
+
+def spork_ngram_workspace_bytes(n_seqs, max_len):
+    b = ctypes.c_size_t()
+    _check(lib().spork_ngram_workspace_bytes(n_seqs, max_len, ctypes.byref(b)))
+    return b.value
+
+
+def spork_ngram_propose(tokens, seq_off, n_seqs, max_len, n_min, n_max, k, drafts, n_drafts, workspace,
+                        stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spork_ngram_propose(_ptr(tokens), _ptr(seq_off), n_seqs, max_len, n_min, n_max, k,
+                                     _ptr(drafts), _ptr(n_drafts), _ptr(workspace), ws_bytes,
+                                     _stream(stream)))
 
 
 # ---- kernel timing ------------------------------------------------------------

@@ -580,3 +580,35 @@ def make_named(name, **kw):
     if name == PREFILL_NAME:
         return make_prefill(**kw)
     return make(name, **kw)
+
+
+def token_histories(n_seqs, lengths, vocab=151936, seed=0, copy_prob=0.35, mean_segment=16):
+    """Token sequences (prompt and output so far) for the n-gram draft
+    proposer: concatenated segments of geometric length (mean
+    ``mean_segment``), each with probability ``copy_prob`` a copy of an
+    earlier span of the same sequence (agent traces repeat tool output, JSON
+    keys and earlier calls), else fresh tokens of Zipf(1.2) rank (frequent
+    tokens recur). ``lengths`` is a list or a (lo, hi) range drawn uniformly.
+    Returns the concatenated int32 tokens and int64 offsets ``[n_seqs + 1]``.
+    Drawn from ``numpy.random.default_rng([42, 8, seed])``."""
+    rng = np.random.default_rng([42, 8, seed])
+    if isinstance(lengths, tuple):
+        lengths = rng.integers(lengths[0], lengths[1] + 1, size=n_seqs)
+    seqs = []
+    for L in lengths:
+        L = int(L)
+        t = np.empty(L, dtype=np.int32)
+        n = 0
+        while n < L:
+            seg = min(int(rng.geometric(1.0 / mean_segment)), L - n)
+            if n >= 2 and rng.random() < copy_prob:
+                src = int(rng.integers(0, n - 1))
+                seg = min(seg, n - src)
+                t[n:n + seg] = t[src:src + seg]
+            else:
+                t[n:n + seg] = (rng.zipf(1.2, size=seg) - 1) % vocab
+            n += seg
+        seqs.append(t)
+    off = np.zeros(n_seqs + 1, dtype=np.int64)
+    off[1:] = np.cumsum([len(s) for s in seqs])
+    return (np.concatenate(seqs) if seqs else np.zeros(0, np.int32)), off

@@ -175,6 +175,26 @@ def test_confidence_error_codes():
     conf(None, 0, 100, 0, None, 0, 0.9, None, None, None, None, None, stream=0)
 
 
+def test_ngram_error_codes():
+    """Bad arguments of spork_ngram_propose fail on the host, before any launch."""
+    ng = spork.spork_ngram_propose
+    for n_min, n_max, k, max_len in ((0, 3, 4, 10), (3, 2, 4, 10), (1, 33, 4, 10), (1, 3, 4097, 10),
+                                     (1, 3, -1, 10), (1, 3, 4, -1), (1, 3, 4, 1 << 31)):
+        with pytest.raises(spork.SporkError) as e:
+            ng(256, 256, 2, max_len, n_min, n_max, k, 256, 256, None, stream=0)
+        assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:                 # NULL tokens
+        ng(None, 256, 2, 10, 1, 3, 4, 256, 256, None, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:                 # no workspace
+        ng(256, 256, 2, 10, 1, 3, 4, 256, 256, None, stream=0)
+    assert e.value.code == spork.SPORK_E_CAPACITY
+    # one 64-bit key per (sequence, 2048-position chunk), at least one chunk
+    for n, L, want in ((0, 10, 0), (3, 0, 24), (3, 2048, 24), (3, 2049, 48), (64, 36864, 64 * 18 * 8)):
+        assert spork.spork_ngram_workspace_bytes(n, L) == want
+    ng(None, None, 0, 0, 1, 3, 4, None, None, None, stream=0)   # nothing to do
+
+
 def _plan_for(wl, groups=None, n_cu=256):
     c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
     for stp in wl.steps:
