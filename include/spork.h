@@ -227,9 +227,11 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
  * -1 (padding after fewer than k_drafts real drafts) never matches.
  * workspace: the attention's workspace followed (at a 256-byte aligned
  * offset) by spork_verify_workspace_bytes; ws_bytes covers both.
- * With a plan the step is three launches on `stream`: argmax (which also
- * zeroes the attention's list cursors), partial attention, then the merge
- * together with the accept. */
+ * With a plan the step is three launches on `stream`. bf16: a kernel that
+ * zeroes the attention's cursors, the partial attention whose workgroups
+ * take the argmax units once their own lists are done, then the merge
+ * together with the accept. fp32: the argmax, the partial attention, the
+ * merge with the accept. */
 int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q,
                         const void* k_cache, const void* v_cache, void* out, float* lse,
                         const void* logits, int32_t logits_dtype, int32_t vocab,

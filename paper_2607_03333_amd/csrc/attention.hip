@@ -455,6 +455,33 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   // The next take's barrier is reached by every wave only after its last
   // reads of this unit's ring slots, table and next_unit.
   }
+  // Verify step: the greedy argmax over the logits fills the tail of the
+  // launch. Workgroups whose lists are done take (row, chunk) units from one
+  // shared cursor, so the compute units that finish early stream the logits
+  // while the last attention units drain.
+  if (a.tail_units > 0) {
+    __syncthreads();  // every wave has read the last list take
+    for (;;) {
+      if (tid == 0) next_unit = atomicAdd(a.cursors + a.n_lists, 1);
+      __syncthreads();
+      const int u = __builtin_amdgcn_readfirstlane(next_unit);
+      if (u >= a.tail_units) break;
+      const int row = u / a.acc.chunks, c = u % a.acc.chunks;
+      uint64_t* key = a.acc.keys + static_cast<size_t>(row) * a.acc.chunks + c;
+      const size_t roff = static_cast<size_t>(row) * a.acc.vocab;
+      if (a.acc.logits_dtype == 1)
+        argmax_unit<uint16_t, 256, false>(static_cast<const uint16_t*>(a.acc.logits) + roff, a.acc.vocab,
+                                          a.acc.chunks, c, key, nullptr);
+      else
+        argmax_unit<float, 256, false>(static_cast<const float*>(a.acc.logits) + roff, a.acc.vocab, a.acc.chunks,
+                                       c, key, nullptr);
+      // The unit ends with thread 0 storing the key and the next take starts
+      // with thread 0 taking a unit: this barrier keeps the two thread-0
+      // regions apart, so the compiler cannot join them across the loop's
+      // back edge into a loop whose waves run different barrier counts.
+      __syncthreads();
+    }
+  }
 }
 
 // --------------------------------------------------------------------------

@@ -362,20 +362,20 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.lse = lse;
   a.part_o = static_cast<float*>(workspace);
   a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
-  // The persistent bf16 kernel needs its list cursors at zero: a verify step
-  // runs the argmax first, which clears them (the accept then rides in the
-  // merge launch); a decode step clears them with a small kernel.
+  // The persistent bf16 kernel needs its cursors at zero (a small kernel
+  // clears them); in a verify step it also runs the argmax units after its
+  // lists, and the accept rides in the merge launch. The fp32 kernel is not
+  // persistent: there the argmax has a launch of its own first.
   const bool persistent = p.shape.persistent;
   const bool verify = acc != nullptr && acc->n_verify > 0;
   int rc = SPORK_OK;
-  if (verify) {
-    a.acc = *acc;
-    a.acc.counters = persistent ? a.cursors : nullptr;
-    a.acc.n_counters = persistent ? p.n_lists : 0;
+  if (verify) a.acc = *acc;
+  if (persistent) {
+    if (verify) a.tail_units = acc->n_verify * (acc->k_drafts + 1) * acc->chunks;
+    rc = hip_status(spork::launch_counter_reset(a.cursors, p.n_lists + 1, stream), "spork_attn_decode (cursor reset)");
+  } else if (verify) {
     rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(a.acc, stream); }),
                     "spork_verify_accept (argmax)");
-  } else if (persistent) {
-    rc = hip_status(spork::launch_counter_reset(a.cursors, p.n_lists, stream), "spork_attn_decode (cursor reset)");
   }
   if (rc != SPORK_OK) return rc;
   rc = hip_status(timed(SPORK_KERNEL_ATTN, stream, [&] { return spork::launch_attn_partial(a, stream); }),

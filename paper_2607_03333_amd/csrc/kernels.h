@@ -47,6 +47,10 @@ struct AttnArgs {
   float* part_ml;  // [n_partials][2] running max (base 2) and sum
   // Verify step: accept units appended to the merge grid (acc.n_verify of them).
   AcceptArgs acc;
+  // Argmax units (row x vocabulary chunk) the persistent bf16 launch works
+  // through after its lists, through cursors[n_lists]; 0 when the argmax has
+  // a launch of its own.
+  int32_t tail_units;
 };
 
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)

@@ -428,7 +428,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   const size_t o_bytes = align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
   p.off_ws_ml = o_bytes;
   p.off_ws_cursors = o_bytes + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
-  p.workspace_bytes = p.off_ws_cursors + align256(static_cast<size_t>(p.n_lists) * sizeof(int32_t));
+  // list cursors, then the cursor of the argmax units a verify launch takes after its lists
+  p.workspace_bytes = p.off_ws_cursors + align256(static_cast<size_t>(p.n_lists + 1) * sizeof(int32_t));
   *out = std::move(p);
   return "";
 }
