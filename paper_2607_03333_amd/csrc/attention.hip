@@ -190,18 +190,21 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   const size_t hkv = static_cast<size_t>(a.hkv);
   const int ntiles = (w.nrows + 15) >> 4;
 
-  // Query operands and row horizons of this wave's tiles.
+  // Query operands, row horizons and partial-result positions of this
+  // wave's tiles.
   bf16x8 qop[RTW][4];
-  int hz[RTW];
+  int hz[RTW], slot[RTW];
   bool own[RTW];
 #pragma unroll
   for (int j = 0; j < RTW; ++j) {
     const int tile = cw + kWgWaves * j;
     own[j] = tile < ntiles;
     const int i = tile * 16 + r16;
+    slot[j] = 0;
     if (own[j] && i < w.nrows) {
       const RowDesc rd = a.rows[it.row_off + w.row0 + i];
       hz[j] = rd.horizon;
+      slot[j] = a.part_slot[w.partial + i];
       const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rd.qidx) * D);
 #pragma unroll
       for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(qp[4 * s + g]);
@@ -438,7 +441,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
       lt += __shfl_xor(lt, 32);
       const int i = (cw + kWgWaves * j) * 16 + r16;
       if (i < w.nrows) {
-        const size_t pr = static_cast<size_t>(w.partial + i);
+        const size_t pr = static_cast<size_t>(slot[j]);
         if (g == 0) {
           a.part_ml[2 * pr] = m[j];
           a.part_ml[2 * pr + 1] = lt;
@@ -620,7 +623,7 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
       lt += __shfl_xor(lt, 32);
       const int i = t * 16 + r16;
       if (i < w.nrows) {
-        const size_t pr = static_cast<size_t>(w.partial + i);
+        const size_t pr = static_cast<size_t>(a.part_slot[w.partial + i]);
         if (g == 0) {
           a.part_ml[2 * pr] = m[t];
           a.part_ml[2 * pr + 1] = lt;
@@ -650,12 +653,12 @@ template <int B, int D>
 __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bool first, int lane, float& run_max,
                                             float& mu, float& sum, float (&acc)[D / 64]) {
   constexpr int PER = D / 64;
-  const int id = a.merge_ids[c0 + min(lane, k - 1)];
-  const float2 ml = reinterpret_cast<const float2*>(a.part_ml)[id];
+  // the output's partials are consecutive: rows c0 .. c0 + k - 1
+  const float2 ml = reinterpret_cast<const float2*>(a.part_ml)[c0 + min(lane, k - 1)];
   float po[B][PER];
 #pragma unroll
   for (int i = 0; i < B; ++i) {
-    const int idi = __builtin_amdgcn_readlane(id, i);
+    const int idi = c0 + min(i, k - 1);
     const float* src = a.part_o + static_cast<size_t>(idi) * D + lane * PER;
 #pragma unroll
     for (int e = 0; e < PER; ++e) po[i][e] = src[e];

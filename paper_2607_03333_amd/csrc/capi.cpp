@@ -341,7 +341,7 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.rows = reinterpret_cast<const spork::RowDesc*>(img + p.off_rows);
   a.tables = reinterpret_cast<const int32_t*>(img + p.off_tables);
   a.merge_off = reinterpret_cast<const int32_t*>(img + p.off_merge_off);
-  a.merge_ids = reinterpret_cast<const int32_t*>(img + p.off_merge_ids);
+  a.part_slot = reinterpret_cast<const int32_t*>(img + p.off_part_slot);
   a.wg_off = reinterpret_cast<const int32_t*>(img + p.off_wg_off);
   a.cursors = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + p.off_ws_cursors);
   a.n_units = p.n_units;

@@ -30,7 +30,7 @@ struct AttnArgs {
   const RowDesc* rows;
   const int32_t* tables;
   const int32_t* merge_off;
-  const int32_t* merge_ids;
+  const int32_t* part_slot;  // merge position of each unit row's partial result
   // Unit lists (CSR over waves): the bf16 kernel's workgroup b takes the units
   // of list b % n_lists in order, through cursors[list] (zero before the launch).
   const int32_t* wg_off;

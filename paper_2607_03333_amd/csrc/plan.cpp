@@ -391,12 +391,15 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     if (count[o + 1] == 0) return "internal: output without a partial";
     count[o + 1] += count[o];
   }
-  std::vector<int32_t> merge_ids(count[p.n_out]);
+  // Each unit row writes its partial result at its output's next merge
+  // position, so the partials of an output sit next to each other and the
+  // merge reads them without an index list.
+  std::vector<int32_t> part_slot(partial);
   std::vector<int32_t> fill(count.begin(), count.end() - 1);
   for (const WaveDesc& w : waves) {
     if (w.item < 0) continue;
     for (int32_t i = 0; i < w.nrows; ++i)
-      merge_ids[fill[rows[items[w.item].row_off + w.row0 + i].qidx]++] = w.partial + i;
+      part_slot[w.partial + i] = fill[rows[items[w.item].row_off + w.row0 + i].qidx]++;
   }
 
   // Device image.
@@ -411,7 +414,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   p.off_rows = place(rows.size() * sizeof(RowDesc));
   p.off_tables = place(tables.size() * sizeof(int32_t));
   p.off_merge_off = place(count.size() * sizeof(int32_t));
-  p.off_merge_ids = place(merge_ids.size() * sizeof(int32_t));
+  p.off_part_slot = place(part_slot.size() * sizeof(int32_t));
   p.off_wg_off = place(wg_off.size() * sizeof(int32_t));
   p.image.assign(off, 0);
   auto put = [&](size_t at, const void* src, size_t bytes) {
@@ -422,7 +425,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   put(p.off_rows, rows.data(), rows.size() * sizeof(RowDesc));
   put(p.off_tables, tables.data(), tables.size() * sizeof(int32_t));
   put(p.off_merge_off, count.data(), count.size() * sizeof(int32_t));
-  put(p.off_merge_ids, merge_ids.data(), merge_ids.size() * sizeof(int32_t));
+  put(p.off_part_slot, part_slot.data(), part_slot.size() * sizeof(int32_t));
   put(p.off_wg_off, wg_off.data(), wg_off.size() * sizeof(int32_t));
 
   const size_t o_bytes = align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));

@@ -36,7 +36,7 @@ struct Plan {
   // device image: sections at 256-byte aligned byte offsets
   std::vector<uint8_t> image;
   size_t off_waves = 0, off_items = 0, off_rows = 0, off_tables = 0, off_merge_off = 0,
-         off_merge_ids = 0, off_wg_off = 0;
+         off_part_slot = 0, off_wg_off = 0;
   size_t workspace_bytes = 0;  // partial outputs + (m, l) pairs + list cursors
   size_t off_ws_ml = 0;        // byte offset of the (m, l) pairs in the workspace
   size_t off_ws_cursors = 0;   // byte offset of the list cursors (zeroed before each launch)

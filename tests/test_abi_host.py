@@ -240,7 +240,7 @@ def _check_cover(wl, c, p):
     through block-table entries equal to the thread's own table."""
     info, img = _decode_image(p)
     raw = img.view(np.int32)
-    # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, merge_ids
+    # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, part_slot
     nw = info["n_units"]
     waves = raw[: nw * 6].reshape(nw, 6)
     off = -(-nw * 24 // 256) * 256 // 4
@@ -270,6 +270,23 @@ def _check_cover(wl, c, p):
                 assert np.all(blk < it[2])
                 assert np.array_equal(tables[it[1] + blk], own[seq][blk]), (seq, lo, top)
     assert len(cover) == sum(stp.n_rows) * wl.hq
+    # the last three sections: merge offsets per output, the merge position
+    # of every unit row's partial, the unit lists
+    al = lambda n: -(-n * 4 // 256) * 256 // 4
+    n_out, n_part = sum(stp.n_rows) * wl.hq, info["n_partials"]
+    n_lists = info["attn_grid"] // 2 if wl.dtype == synth.BF16 else info["attn_grid"]
+    o_wg = info["image_bytes"] // 4 - al(n_lists + 1)
+    o_ps = o_wg - al(n_part)
+    o_mo = o_ps - al(n_out + 1)
+    merge_off, part_slot = raw[o_mo: o_mo + n_out + 1], raw[o_ps: o_ps + n_part]
+    assert np.array_equal(np.sort(part_slot), np.arange(n_part))   # every position written once
+    for w in waves:
+        item, lo, hi, row0, nr, part = (int(x) for x in w)
+        if item < 0:
+            continue
+        for i in range(nr):
+            o = int(rows[items[item][3] + row0 + i][0])
+            assert merge_off[o] <= part_slot[part + i] < merge_off[o + 1]
     row = 0
     lens = {s: spork.spork_seq_len(c, s) for s in stp.seqs}
     for s, n in zip(stp.seqs, stp.n_rows):
