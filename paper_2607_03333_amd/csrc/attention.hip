@@ -76,9 +76,16 @@ __device__ __forceinline__ float softmax_step(float (&sv)[8], float& m, float& l
 //   lane's own 8 probabilities; the accumulator holds query row r16 at
 //   channels 16*dt + 4g + i, so the rescale by the row's factor is lane-local.
 // --------------------------------------------------------------------------
-constexpr int kWgWaves = 4;
 constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 bytes / 16
-constexpr int kRing = 4;            // LDS stages per workgroup (kRing - 1 in flight)
+// LDS stages per workgroup (ring_of - 1 in flight): 4 for two 4-wave
+// workgroups on a compute unit, 8 for one 8-wave workgroup.
+template <int NW>
+constexpr int ring_of() { return NW == 4 ? 4 : 8; }
+
+// Wait until at most `after` stages of this wave's direct-to-LDS loads (LPW
+// per stage) are still in flight.
+template <int RING, int LPW>
+__device__ __forceinline__ void wait_stage(int after);
 constexpr int kUnitBlocks = 1040;   // block-table entries a unit may span (see kMaxUnitTokens)
 constexpr float kRescaleSlack = 8.0f;  // base-2 headroom before the reference max moves
 constexpr float kRescaleSum = 256.0f;  // 2^kRescaleSlack: bound on a lane's 8 probabilities of a row
@@ -150,10 +157,34 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int RTW, int BS>
-__global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
+template <int RING, int LPW>
+__device__ __forceinline__ void wait_stage(int after) {
+  if constexpr (RING == 4 && LPW == 4) {
+    if (after >= 2) wait_vmcnt<8>();
+    else if (after == 1) wait_vmcnt<4>();
+    else wait_vmcnt<0>();
+  } else {
+    static_assert(RING == 8 && LPW == 2, "ring shapes with a wait ladder");
+    switch (after) {
+      case 6: wait_vmcnt<12>(); break;
+      case 5: wait_vmcnt<10>(); break;
+      case 4: wait_vmcnt<8>(); break;
+      case 3: wait_vmcnt<6>(); break;
+      case 2: wait_vmcnt<4>(); break;
+      case 1: wait_vmcnt<2>(); break;
+      default: wait_vmcnt<0>(); break;
+    }
+  }
+}
+
+template <int RTW, int BS, int NW>
+__global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs a) {
   constexpr int D = 128;
+  constexpr int kRing = ring_of<NW>();
+  constexpr int LPW = 16 / NW;  // direct-to-LDS loads per wave per 16 KB stage
+  constexpr int NT_ = 64 * NW;  // threads
   static_assert(BS == 16 || BS == 32, "unsupported block size");
+  static_assert(NW == 4 || NW == 8, "workgroups of 4 or 8 waves");
   __shared__ uint4 smem[kRing][kStageChunks];
   __shared__ int tab[kUnitBlocks];
   __shared__ int next_unit;
@@ -179,7 +210,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   // one): wave w of both shares SIMD w, and with 5-7 tiles (two for some
   // waves, one for others) the rotation pairs each wave holding two tiles
   // with one holding one.
-  const int cw = (wave + 2 * (static_cast<int>(blockIdx.x) / a.n_lists)) & (kWgWaves - 1);
+  const int cw = NW == 4 ? (wave + 2 * (static_cast<int>(blockIdx.x) / a.n_lists)) & 3 : wave;
   const int lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ qg = static_cast<const uint16_t*>(a.q);
   const uint16_t* __restrict__ kc = static_cast<const uint16_t*>(a.k_cache);
@@ -197,7 +228,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   bool own[RTW];
 #pragma unroll
   for (int j = 0; j < RTW; ++j) {
-    const int tile = cw + kWgWaves * j;
+    const int tile = cw + NW * j;
     own[j] = tile < ntiles;
     const int i = tile * 16 + r16;
     slot[j] = 0;
@@ -239,12 +270,12 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   // (4w + k)*64 + lane. Waves 0-1: K chunks (token t, channel group c);
   // waves 2-3: V chunks (channel d, token octet q). The element offset inside
   // a block and the block (first or second of the stage) are fixed per lane.
-  size_t off[4];
-  bool second[4];
+  size_t off[LPW];
+  bool second[LPW];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int chunk = (4 * wave + k) * 64 + lane;
-    if (wave < 2) {
+  for (int k = 0; k < LPW; ++k) {
+    const int chunk = (LPW * wave + k) * 64 + lane;
+    if (wave < NW / 2) {
       const int t = chunk >> 4;
       const int cg = (chunk & 15) ^ k_swz(t);
       second[k] = BS == 16 && t >= 16;
@@ -256,8 +287,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
       off[k] = static_cast<size_t>(d) * BS + (8 * q) % BS;
     }
   }
-  const uint16_t* pool = wave < 2 ? kc : vc;
-  static_assert(kRing - 2 == 2, "the vmcnt ladder below assumes two stages in flight behind the current one");
+  const uint16_t* pool = wave < NW / 2 ? kc : vc;
   // The unit's slice of the block table, staged in LDS before the ring
   // starts (tab[i] = table entry tb0/BS + i, clamped to the table) and read
   // per stage outside the compiler's view (a vector load of the table inside
@@ -265,7 +295,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
   // issued before it).
   const int tab0 = tb0 / BS;
   const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
-  for (int i = tid; i < ntab; i += 256) {
+  for (int i = tid; i < ntab; i += NT_) {
     const int bi = tab0 + i;
     tab[i] = table[bi < nb ? bi : nb - 1];
   }
@@ -279,9 +309,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
     const size_t base1 = (static_cast<size_t>(e1) * hkv + head) * (static_cast<size_t>(BS) * D);
     uint4* slot = smem[st % kRing];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < LPW; ++k) {
       const uint16_t* src = pool + (second[k] ? base1 : base0) + off[k];
-      __builtin_amdgcn_global_load_lds((global_void_ptr)src, (lds_void_ptr)(slot + (4 * wave + k) * 64), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_void_ptr)src, (lds_void_ptr)(slot + (LPW * wave + k) * 64), 16, 0, 0);
     }
   };
 
@@ -425,11 +455,8 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
     constexpr int NT = decltype(nt_c)::value;
     for (int st = 0; st < nstage; ++st) {
       // Wait for this wave's loads of stage st: the stages issued after it
-      // (at most kRing - 2 of them, 4 loads each) may stay in flight.
-      const int after = min(kRing - 2, nstage - 1 - st);
-      if (after >= 2) wait_vmcnt<8>();
-      else if (after == 1) wait_vmcnt<4>();
-      else wait_vmcnt<0>();
+      // (at most kRing - 2 of them, LPW loads each) may stay in flight.
+      wait_stage<kRing, LPW>(min(kRing - 2, nstage - 1 - st));
       barrier_nofence();  // stage st visible to all waves; slot of stage st-1 free
       if (st + kRing - 1 < nstage) issue_stage(st + kRing - 1);
       if constexpr (NT > 0) compute_tiles(nt_c, st);
@@ -439,7 +466,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
     for (int j = 0; j < NT; ++j) {
       float lt = l[j] + __shfl_xor(l[j], 16);
       lt += __shfl_xor(lt, 32);
-      const int i = (cw + kWgWaves * j) * 16 + r16;
+      const int i = (cw + NW * j) * 16 + r16;
       if (i < w.nrows) {
         const size_t pr = static_cast<size_t>(slot[j]);
         if (g == 0) {
@@ -473,10 +500,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16(AttnArgs a) {
       uint64_t* key = a.acc.keys + static_cast<size_t>(row) * a.acc.chunks + c;
       const size_t roff = static_cast<size_t>(row) * a.acc.vocab;
       if (a.acc.logits_dtype == 1)
-        argmax_unit<uint16_t, 256, false>(static_cast<const uint16_t*>(a.acc.logits) + roff, a.acc.vocab,
+        argmax_unit<uint16_t, NT_, false>(static_cast<const uint16_t*>(a.acc.logits) + roff, a.acc.vocab,
                                           a.acc.chunks, c, key, nullptr);
       else
-        argmax_unit<float, 256, false>(static_cast<const float*>(a.acc.logits) + roff, a.acc.vocab, a.acc.chunks,
+        argmax_unit<float, NT_, false>(static_cast<const float*>(a.acc.logits) + roff, a.acc.vocab, a.acc.chunks,
                                        c, key, nullptr);
       // The unit ends with thread 0 storing the key and the next take starts
       // with thread 0 taking a unit: this barrier keeps the two thread-0
@@ -731,11 +758,11 @@ __global__ void __launch_bounds__(256) counter_reset_kernel(int32_t* counters, i
 // --------------------------------------------------------------------------
 typedef void (*AttnKernel)(AttnArgs);
 
-template <int BS>
+template <int BS, int NW>
 AttnKernel pick_bf16(int row_tiles) {
-  switch ((row_tiles + kWgWaves - 1) / kWgWaves) {
-    case 1: return attn_bf16<1, BS>;
-    case 2: return attn_bf16<2, BS>;
+  switch ((row_tiles + NW - 1) / NW) {
+    case 1: return attn_bf16<1, BS, NW>;
+    case 2: return attn_bf16<2, BS, NW>;
     default: return nullptr;
   }
 }
@@ -751,10 +778,10 @@ AttnKernel pick_f32(int rt) {
   }
 }
 
-AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt) {
-  if (dtype == 1 && d == 128) {
-    if (bs == 16) return pick_bf16<16>(rt);
-    if (bs == 32) return pick_bf16<32>(rt);
+AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt, int32_t waves) {
+  if (dtype == 1 && d == 128 && (waves == 4 || waves == 8)) {
+    if (bs == 16) return waves == 4 ? pick_bf16<16, 4>(rt) : pick_bf16<16, 8>(rt);
+    if (bs == 32) return waves == 4 ? pick_bf16<32, 4>(rt) : pick_bf16<32, 8>(rt);
   }
   if (dtype == 0) {
     if (d == 64 && bs == 16) return pick_f32<64, 16>(rt);
@@ -767,14 +794,14 @@ AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt) {
 
 }  // namespace
 
-bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles) {
-  return pick_attention(dtype, head_dim, block_size, row_tiles) != nullptr;
+bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles, int32_t waves) {
+  return pick_attention(dtype, head_dim, block_size, row_tiles, waves) != nullptr;
 }
 
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream) {
-  AttnKernel k = pick_attention(a.dtype, a.head_dim, a.block_size, a.row_tiles);
+  AttnKernel k = pick_attention(a.dtype, a.head_dim, a.block_size, a.row_tiles, a.wg_waves);
   if (k == nullptr) return hipErrorInvalidValue;
-  const int threads = a.dtype == 1 ? 64 * kWgWaves : 64;
+  const int threads = a.dtype == 1 ? 64 * a.wg_waves : 64;
   if (a.grid > 0) hipLaunchKernelGGL(k, dim3(a.grid), dim3(threads), 0, stream, a);
   return hipGetLastError();
 }

@@ -265,15 +265,26 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
       return fail(SPORK_E_INVAL, "NULL argument");
     int rc = check_shape(shape);
     if (rc != SPORK_OK) return rc;
-    // bf16: persistent 4-wave workgroups with up to 2 row tiles per wave,
-    // 2 per CU (their 68 KB of LDS); fp32: one 1-wave workgroup per unit with
-    // up to 4 row tiles, 4 per CU (8 with up to 2 tiles).
+    // bf16: persistent 4-wave workgroups with up to 2 row tiles per wave, two
+    // per compute unit (68 KB of LDS each). When some range has more than 16
+    // row tiles (multi-row probe prefill, verify at K of about 50), the batch
+    // is MFMA-bound and 4-wave workgroups would stream that range in three or
+    // more row slices: it is planned again for one 8-wave workgroup per
+    // compute unit (up to 16 tiles, an 8-stage 128 KB ring). fp32: one 1-wave
+    // workgroup per unit with up to 4 row tiles, 4 per CU (8 with up to 2).
     const bool bf16 = shape->dtype == SPORK_DTYPE_BF16;
-    spork::PlanShape ps{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype),
-                        bf16 ? 8 : 4, bf16 ? 2 : 4, bf16 ? 2 : 8, bf16};
+    auto shape_for = [&](int32_t waves) {
+      return spork::PlanShape{shape->hq, shape->hkv, shape->head_dim, shape->block_size, elem_bytes(shape->dtype),
+                              bf16 ? 2 * waves : 4, bf16 ? 8 / waves : 4, bf16 ? 8 / waves : 8, bf16,
+                              bf16 ? waves : 1};
+    };
     auto* plan = new spork_plan();
     plan->shape = *shape;
-    const std::string err = spork::build_plan(cache->bm, ps, seqs, n_rows, groups, n_threads, n_cu, &plan->p);
+    std::string err = spork::build_plan(cache->bm, shape_for(4), seqs, n_rows, groups, n_threads, n_cu, &plan->p);
+    if (err.empty() && bf16 && plan->p.max_range_tiles > 16) {
+      plan->p = spork::Plan{};
+      err = spork::build_plan(cache->bm, shape_for(8), seqs, n_rows, groups, n_threads, n_cu, &plan->p);
+    }
     if (!err.empty()) {
       delete plan;
       return fail(SPORK_E_INVAL, "spork_plan_create: " + err);
@@ -300,6 +311,7 @@ int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info) {
   info->attn_grid = p.grid;
   info->n_partials = p.n_partials;
   info->max_row_tiles = p.row_tiles;
+  info->attn_waves = p.shape.waves;
   info->image_bytes = p.image.size();
   info->workspace_bytes = p.workspace_bytes;
   info->shared_tokens = p.shared_tokens;
@@ -324,7 +336,7 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
                      const spork::AcceptArgs* acc, hipStream_t stream) {
   const spork::Plan& p = plan->p;
   const spork_shape& sh = plan->shape;
-  if (!spork::attention_supported(sh.dtype, sh.head_dim, sh.block_size, p.row_tiles))
+  if (!spork::attention_supported(sh.dtype, sh.head_dim, sh.block_size, p.row_tiles, p.shape.waves))
     return fail(SPORK_E_UNSUPPORTED, "no attention kernel for this dtype / head_dim / block_size / row tiles "
                                      "(bf16: head_dim 128; f32: head_dim 64 or 128; block_size 16 or 32)");
   if (!dev_image || !q || !k_cache || !v_cache || !out) return fail(SPORK_E_INVAL, "NULL pointer");
@@ -349,6 +361,7 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.n_lists = p.n_lists;
   a.n_out = p.n_out;
   a.row_tiles = p.row_tiles;
+  a.wg_waves = p.shape.waves;
   a.hq = sh.hq;
   a.hkv = sh.hkv;
   a.head_dim = sh.head_dim;

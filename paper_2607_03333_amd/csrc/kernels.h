@@ -36,6 +36,9 @@ struct AttnArgs {
   const int32_t* wg_off;
   int32_t* cursors;
   int32_t n_units, grid, n_lists, n_out, row_tiles;
+  // waves of a bf16 workgroup: 4 (two persistent workgroups per compute unit,
+  // up to 8 row tiles each) or 8 (one per compute unit, up to 16)
+  int32_t wg_waves;
   int32_t hq, hkv, head_dim, block_size, dtype;
   float scale_log2;  // sm_scale * log2(e): scores are kept in base 2
   const void* q;
@@ -54,7 +57,7 @@ struct AttnArgs {
 };
 
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
-bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles);
+bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles, int32_t waves);
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream);
 // zero n int32 counters (the list cursors, before a persistent attention launch)
 hipError_t launch_counter_reset(int32_t* counters, int32_t n, hipStream_t stream);

@@ -152,6 +152,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     for (int32_t t : ranges[r].threads) rows += n_rows[t] * gq;
     range_rows[r] = rows;
     const int32_t tiles = (rows + 15) / 16;
+    p.max_range_tiles = std::max(p.max_range_tiles, tiles);
     const int32_t slices = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
     row_tiles = std::max(row_tiles, (tiles + slices - 1) / slices);
   }

@@ -25,6 +25,7 @@ struct PlanShape {
   int32_t units_per_cu;    // attention workgroups resident per compute unit
   int32_t units_per_cu_half;  // the same when every workgroup needs at most half the tiles
   bool persistent;         // resident workgroups each work through a list of units
+  int32_t waves;           // waves per workgroup (bf16: 4 or 8; fp32: 1)
 };
 
 struct Plan {
@@ -32,6 +33,7 @@ struct Plan {
   int32_t n_threads = 0, n_rows = 0, n_groups = 0, n_items = 0;
   int32_t n_units = 0, grid = 0, n_partials = 0, row_tiles = 1, n_out = 0;
   int32_t n_lists = 0;  // unit lists (persistent launch: one per compute unit)
+  int32_t max_range_tiles = 0;  // 16-row tiles of the largest range's row set, before slicing
   int64_t shared_tokens = 0, private_tokens = 0, flat_tokens = 0;
   // device image: sections at 256-byte aligned byte offsets
   std::vector<uint8_t> image;

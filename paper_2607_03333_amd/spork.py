@@ -59,7 +59,7 @@ class spork_plan_info(ctypes.Structure):
                 ("max_row_tiles", _c_i32), ("attn_grid", _c_i32),
                 ("image_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
                 ("shared_tokens", _c_i64), ("private_tokens", _c_i64),
-                ("unique_kv_bytes", _c_i64), ("flat_kv_bytes", _c_i64)]
+                ("unique_kv_bytes", _c_i64), ("flat_kv_bytes", _c_i64), ("attn_waves", _c_i32)]
 
 
 # name -> (restype, argtypes); every name is declared in include/spork.h

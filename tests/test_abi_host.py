@@ -274,7 +274,7 @@ def _check_cover(wl, c, p):
     # of every unit row's partial, the unit lists
     al = lambda n: -(-n * 4 // 256) * 256 // 4
     n_out, n_part = sum(stp.n_rows) * wl.hq, info["n_partials"]
-    n_lists = info["attn_grid"] // 2 if wl.dtype == synth.BF16 else info["attn_grid"]
+    n_lists = info["attn_grid"] // 2 if info["attn_waves"] == 4 else info["attn_grid"]
     o_wg = info["image_bytes"] // 4 - al(n_lists + 1)
     o_ps = o_wg - al(n_part)
     o_mo = o_ps - al(n_out + 1)
@@ -371,7 +371,9 @@ def test_plan_lists(index, n_cu, shrink):
     raw = img.view(np.int32)
     nu, grid = info["n_units"], info["attn_grid"]
     bf16 = wl.dtype == synth.BF16
-    assert grid == (2 * n_cu if bf16 else nu)
+    per_cu = 2 if info["attn_waves"] == 4 else 1
+    assert info["attn_waves"] == (4 if bf16 else 1)
+    assert grid == (per_cu * n_cu if bf16 else nu)
     n_lists = n_cu if bf16 else nu
     off = (info["image_bytes"] - (-(-(n_lists + 1) * 4 // 256) * 256)) // 4
     wg_off = raw[off: off + n_lists + 1]
@@ -430,6 +432,10 @@ def test_probe_prefill_plan(shape):
     assert info["unique_kv_bytes"] == wl.unique_kv_bytes(0)
     forks = [t.fork_len for t in wl.threads if t.role == "probe"][::2]
     assert info["shared_tokens"] == sum(f // wl.block_size * wl.block_size for f in forks)
+    if wl.dtype == synth.BF16:
+        # openers of up to 50 rows: a shared range of up to 101 rows x 8 heads,
+        # planned for 8-wave workgroups, one per compute unit
+        assert info["attn_waves"] == 8 and info["attn_grid"] == 8 and info["max_row_tiles"] <= 16
     _check_cover(wl, c, p)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)
