@@ -147,3 +147,28 @@ def test_verify_k50():
     wl = synth.make(3, sessions=3, prefix=600, verify_k=50, vocab=2000)
     dw = run_workload(wl, "verify k50")
     dw.close()
+
+
+@pytest.mark.parametrize("index,shrink", [
+    (0, dict(block_size=32)),                                                           # fp32 decode + verify
+    (4, dict(sessions=3, prefix=1000, suffix=("loguniform", 1, 400), vocab=3000, block_size=32)),
+    (2, dict(sessions=2, prefix=777, suffix=("uniform", 1, 200), block_size=32)),      # fork inside a block
+])
+def test_block_size_32(index, shrink):
+    wl = synth.make(index, **shrink)
+    say(f"block size 32: {wl.name}")
+    run_workload(wl, f"{wl.name}-bs32").close()
+
+
+def test_staggered_tree_block_size_32():
+    wl = synth.make_tree(sessions=2, prefix=640, stride=50, probes=3, probe_tokens=(1, 40), main_extra=(1, 60),
+                         block_size=32)
+    say("staggered tree, block size 32")
+    run_workload(wl, "tree-bs32").close()
+
+
+def test_probe_prefill_block_size_32():
+    # more than 16 row tiles in the shared range: 8-wave workgroups, 32-token blocks
+    wl = synth.make_prefill(sessions=2, prefix=700, cot=("uniform", 1, 300), opener=(40, 50), block_size=32)
+    say("probe prefill, block size 32")
+    run_workload(wl, "prefill-bs32").close()
