@@ -172,3 +172,13 @@ def test_probe_prefill_block_size_32():
     wl = synth.make_prefill(sessions=2, prefix=700, cot=("uniform", 1, 300), opener=(40, 50), block_size=32)
     say("probe prefill, block size 32")
     run_workload(wl, "prefill-bs32").close()
+
+
+@pytest.mark.parametrize("block_size", [16, 32])
+def test_fp32_head_dim_128(block_size):
+    # fp32 with 128-channel heads: the fp32 kernel's D = 128 instances, several
+    # row slices of up to 4 tiles, and the fp32 merge at D = 128
+    wl = synth.make_prefill(sessions=2, prefix=300, cot=("uniform", 1, 100), opener=(8, 30), hq=8, hkv=2, d=128,
+                            dtype=synth.F32, block_size=block_size)
+    say(f"fp32 head dim 128, block size {block_size}")
+    run_workload(wl, f"f32-d128-bs{block_size}").close()
