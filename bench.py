@@ -275,6 +275,9 @@ def main():
             elif op[0] == "append":
                 spork.spork_seq_append(cache, op[1], op[2])
                 t_other += time.perf_counter() - t
+            elif op[0] == "free":
+                spork.spork_seq_free(cache, op[1])
+                t_other += time.perf_counter() - t
             else:
                 spork.spork_fork(cache, op[1])
                 t_fork += time.perf_counter() - t

@@ -131,6 +131,8 @@ class DeviceWorkload:
                 spork.spork_kv_write(self.shape, self.k_pool, self.v_pool, wl.num_blocks, sd, kd, vd,
                                      self.bad_slots)
                 self.written[seq] = lo + n
+            elif op[0] == "free":
+                spork.spork_seq_free(self.cache, op[1])
             else:
                 raise ValueError(op)
 

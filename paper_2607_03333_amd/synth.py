@@ -612,3 +612,49 @@ def token_histories(n_seqs, lengths, vocab=151936, seed=0, copy_prob=0.35, mean_
     off = np.zeros(n_seqs + 1, dtype=np.int64)
     off[1:] = np.cumsum([len(s) for s in seqs])
     return (np.concatenate(seqs) if seqs else np.zeros(0, np.int32)), off
+
+
+def add_supersession_step(wl, more=(20, 120), own=(4, 30), seed=0):
+    """A second step for a fork tree: the controller probes again while the
+    earlier probes still run (the late-probe supersession of the paper's
+    appendix, Algorithm 1's next retry). In every session the oldest live
+    probe is freed (its blocks go back to the free queue, holding stale KV),
+    the main thread decodes ``more`` further tokens (uniform) and a new probe
+    forks at that point and appends ``own`` tokens (uniform). The step decodes
+    one row for the main thread, the surviving probes and the new one. Drawn
+    from ``numpy.random.default_rng([42, 9, seed])``; the new tokens' K and V
+    from ``[42, 9, seed, seq]``."""
+    rng = np.random.default_rng([42, 9, seed])
+    prev = wl.steps[-1]
+    si = len(wl.steps) - 1
+    nid = max(t.seq for t in wl.threads) + 1
+    hkv, d, dtype = wl.hkv, wl.d, wl.dtype
+
+    def kv(key, n):
+        r = np.random.default_rng([42, 9, seed, key])
+        return (to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype),
+                to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype))
+
+    ops, seqs = [], []
+    for m in [t for t in wl.threads if t.role == "main" and t.seq in prev.seqs]:
+        live = [t for t in wl.threads if t.role == "probe" and t.session == m.session and t.seq in prev.seqs]
+        if live:
+            ops.append(("free", live[0].seq))
+        add = int(rng.integers(more[0], more[1] + 1))
+        length = wl.thread_len(m.seq, si)
+        k, v = kv(m.seq, add)
+        wl.suffix_k[m.seq] = np.concatenate([wl.suffix_k[m.seq], k])
+        wl.suffix_v[m.seq] = np.concatenate([wl.suffix_v[m.seq], v])
+        m.suffix += add
+        ops.append(("append", m.seq, add))
+        n_own = int(rng.integers(own[0], own[1] + 1))
+        t = Thread(seq=nid, session=m.session, role="probe", suffix=n_own, parent=m.seq, fork_len=length + add)
+        wl.threads.append(t)
+        wl.suffix_k[nid], wl.suffix_v[nid] = kv(nid, n_own)
+        ops += [("fork", m.seq, nid), ("append", nid, n_own)]
+        seqs += [m.seq] + [p.seq for p in live[1:]] + [nid]
+        nid += 1
+    q = to_storage(rng.standard_normal((len(seqs), wl.hq, d), dtype=np.float32), dtype)
+    groups = [wl.thread(s).session for s in seqs]
+    wl.steps.append(Step(seqs=seqs, n_rows=[1] * len(seqs), groups=groups, q=q, ops_before=ops))
+    return wl

@@ -91,6 +91,8 @@ def compare_tables(wl, dw):
                 bm.seq_new()
             elif op[0] == "append":
                 bm.append(op[1], op[2])
+            elif op[0] == "free":
+                bm.free_seq(op[1])
             else:
                 bm.fork(op[1])
     for s in bm.tables:

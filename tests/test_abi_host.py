@@ -203,6 +203,8 @@ def _plan_for(wl, groups=None, n_cu=256):
                 spork.spork_seq_new(c)
             elif op[0] == "append":
                 spork.spork_seq_append(c, op[1], op[2])
+            elif op[0] == "free":
+                spork.spork_seq_free(c, op[1])
             else:
                 spork.spork_fork(c, op[1])
     stp = wl.steps[-1]
@@ -436,6 +438,20 @@ def test_probe_prefill_plan(shape):
         # openers of up to 50 rows: a shared range of up to 101 rows x 8 heads,
         # planned for 8-wave workgroups, one per compute unit
         assert info["attn_waves"] == 8 and info["attn_grid"] == 8 and info["max_row_tiles"] <= 16
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+def test_supersession_plan():
+    """The step after a probe is freed and a new one forked: the plan's unique
+    bytes and coverage hold on the reused blocks."""
+    wl = synth.make_tree(sessions=3, prefix=300, stride=40, probes=3, probe_tokens=(1, 20), main_extra=(1, 30),
+                         hq=4, hkv=2, d=64, dtype=synth.F32)
+    synth.add_supersession_step(wl, seed=2)
+    c, p = _plan_for(wl, n_cu=8)
+    info = spork.spork_plan_get_info(p)
+    assert info["unique_kv_bytes"] == wl.unique_kv_bytes(1)
     _check_cover(wl, c, p)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)

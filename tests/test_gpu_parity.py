@@ -182,3 +182,16 @@ def test_fp32_head_dim_128(block_size):
                             dtype=synth.F32, block_size=block_size)
     say(f"fp32 head dim 128, block size {block_size}")
     run_workload(wl, f"f32-d128-bs{block_size}").close()
+
+
+@pytest.mark.parametrize("dtype,shape", [(synth.F32, dict(hq=4, hkv=2, d=64)), (synth.BF16, dict())])
+def test_supersession_frees_and_reforks(dtype, shape):
+    """A second step after a fork tree: the oldest probe of every session is
+    freed (its blocks return to the free queue with stale KV), the main thread
+    decodes on and a new probe forks; both steps match the oracle and the
+    block tables and free queue match the oracle manager."""
+    wl = synth.make_tree(sessions=3, prefix=500, stride=40, probes=3, probe_tokens=(1, 30), main_extra=(1, 40),
+                         dtype=dtype, **shape)
+    synth.add_supersession_step(wl, seed=1)
+    say(f"supersession {dtype}: step 1 ops {wl.steps[1].ops_before[:4]}")
+    run_workload(wl, f"supersede {dtype}").close()
