@@ -38,10 +38,14 @@ def _pick(wl, step_index):
 
 
 @pytest.mark.parametrize("index,over", [(0, {}), (1, {}), (2, {}), (3, {}), (4, {}), (synth.TREE_NAME, {}),
-                                        (synth.PREFILL_NAME, {}), ("qwen3-32b-verify", dict(verify_k=50))],
-                         ids=["0", "1", "2", "3", "4", "tree", "prefill", "verify-k50"])
+                                        (synth.PREFILL_NAME, {}), ("qwen3-32b-verify", dict(verify_k=50)),
+                                        ("supersede", {})],
+                         ids=["0", "1", "2", "3", "4", "tree", "prefill", "verify-k50", "tree-supersede"])
 def test_full_size_workload(index, over):
-    wl = synth.make_named(index, **over)
+    if index == "supersede":
+        wl = synth.add_supersession_step(synth.make_tree())
+    else:
+        wl = synth.make_named(index, **over)
     say(f"[full {wl.name}] generated; blocks {wl.num_blocks}")
     dw = runner.DeviceWorkload(wl, poison_pool=True)
     try:
