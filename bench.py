@@ -31,6 +31,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "forked decode-attn unique-KV GB/s (% of 8 TB/s) + verified tokens/s"
 HBM_PEAK_GBPS = 8000.0
+# Dense MFMA peaks of MI355X (no sparsity), TFLOP/s, by the kernel's operand type.
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 DEFAULT_WORKLOAD = "qwen3-30b-a3b-mixed"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_partial_traffic.json")
 # the attention kernel's source and every header it includes
@@ -56,6 +58,19 @@ def measured_traffic(workload):
     if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("bytes_per_launch")
+
+
+def attention_flops(wl, index, spec):
+    """Algorithmic flops of one step's attention: Q.K^T and P.V cost 2 D
+    flops each per (query-head row, visible position). A thread's rows are
+    the last positions of its context, each seeing the positions up to its
+    own (causal)."""
+    total = 0
+    for seq, r in zip(spec.seqs, spec.n_rows):
+        n = wl.thread_len(seq, index)
+        visible = r * (n - r + 1) + r * (r - 1) // 2
+        total += visible
+    return total * wl.hq * 4 * wl.d
 
 
 def cpu_baseline(wl, step_specs, target_s):
@@ -341,6 +356,30 @@ def main():
     attn_bytes_per_launch = (unique + fused_logits) / len(steps)
     achieved = attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9
     traffic = measured_traffic(wl.name)
+    flops_per_launch = sum(attention_flops(wl, s.index, s.spec) for s in steps) / len(steps)
+    dt = "bf16" if wl.dtype == synth.BF16 else "f32"
+    intensity = flops_per_launch / attn_bytes_per_launch
+    ridge = MFMA_PEAK_TFLOPS[dt] * 1e12 / (HBM_PEAK_GBPS * 1e9)
+    if intensity > ridge:
+        # past the ridge point the launch is priced against the matrix cores
+        tflops = flops_per_launch / (attn_avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": "attn_partial", "achieved": round(tflops, 1),
+                "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s", "frac": round(tflops / MFMA_PEAK_TFLOPS[dt], 4),
+                "traffic": traffic}
+    else:
+        roof = {"bound": "hbm", "kernel": "attn_partial", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": traffic}
+    roof.update({
+        "avg_launch_ms": round(attn_avg_ms, 4),
+        "algorithmic_bytes_per_launch": attn_bytes_per_launch,
+        "algorithmic_bytes": "unique KV" + (" + verify logits (argmax inside the launch)" if fused_logits else ""),
+        "hbm_gbps": round(achieved, 1),
+        "algorithmic_flops_per_launch": flops_per_launch,
+        "tflops": round(flops_per_launch / (attn_avg_ms * 1e-3) / 1e12, 1),
+        "intensity_flop_per_byte": round(intensity, 1),
+        "ridge_flop_per_byte": round(ridge, 1),
+    })
 
     result = {
         "metric": METRIC,
@@ -353,7 +392,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if wl.dtype == synth.BF16 else "f32",
+        "dtype": dt,
         "data": "synthetic (seeded Gaussian K/V/Q" + (", planted greedy logits)" if logits_bytes else ")"),
         "config": {
             "workload": wl.name, "query_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.d,
@@ -373,18 +412,7 @@ def main():
         "host_ms": {"forks": round(t_fork * 1e3, 3), "n_forks": n_forks, "appends_and_new": round(t_other * 1e3, 3),
                     "plan": round(t_plan * 1e3, 3)},
         "wall_s_timed_region": round(wall, 4),
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "attn_partial",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
-            "avg_launch_ms": round(attn_avg_ms, 4),
-            "algorithmic_bytes_per_launch": attn_bytes_per_launch,
-            "algorithmic_bytes": "unique KV" + (" + verify logits (argmax inside the launch)" if fused_logits else ""),
-        },
+        "roofline": roof,
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, [(s.index, s.spec) for s in steps], args.cpu_seconds)

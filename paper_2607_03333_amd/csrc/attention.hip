@@ -371,36 +371,41 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     vr[5] = lds_read_b128<5 * 1024>(va);
     vr[6] = lds_read_b128<6 * 1024>(va);
     vr[7] = lds_read_b128<7 * 1024>(va);
-    bf16x8 pop[NT];
+    float sv[NT][8];
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      float sv[8] = {sc[j][0][0], sc[j][0][1], sc[j][0][2], sc[j][0][3],
-                     sc[j][1][0], sc[j][1][1], sc[j][1][2], sc[j][1][3]};
-      if (edge) {
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int tk = tb + 8 * g + e;
-          if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[e] = kNegInf;
-        }
+      for (int e = 0; e < 8; ++e) sv[j][e] = sc[j][e >> 2][e & 3];
+    // Masking of positions outside the range or past a row's horizon (first
+    // and last stages of a unit, causal rows).
+    auto mask_tile = [&](int j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int tk = tb + 8 * g + e;
+        if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[j][e] = kNegInf;
       }
-      // Common case: the lane's 8 probabilities of the row, taken against
-      // the row's reference, sum to at most 2^kRescaleSlack (which bounds
-      // each of them). Only when some lane of the wave sums past that, or a
-      // row has no reference yet, are the row maxima reduced across lanes,
-      // the reference moved where it lags by more than kRescaleSlack (rows
-      // that did not trigger keep theirs) and the probabilities recomputed.
+    };
+    // Softmax of tile j: the lane's 8 probabilities of its row against the
+    // row's reference. Common case: they sum to at most 2^kRescaleSlack
+    // (which bounds each of them). Only when some lane of the wave sums past
+    // that, or a row has no reference yet, are the row maxima reduced across
+    // lanes, the reference moved where it lags by more than kRescaleSlack
+    // (rows that did not trigger keep theirs) and the probabilities
+    // recomputed.
+    auto softmax_tile = [&](int j) __attribute__((always_inline)) {
       float ps = 0.0f;
       float pv[8];
       {
         const float mu = m[j] == kNegInf ? 0.0f : m[j];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
+          pv[e] = exp2_fast(__builtin_fmaf(sv[j][e], c, -mu));
           ps += pv[e];
         }
       }
       if (__ballot(!(ps <= kRescaleSum) || m[j] == kNegInf) != 0) {
-        float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])), fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+        float mx = fmaxf(fmaxf(fmaxf(sv[j][0], sv[j][1]), fmaxf(sv[j][2], sv[j][3])),
+                         fmaxf(fmaxf(sv[j][4], sv[j][5]), fmaxf(sv[j][6], sv[j][7])));
         mx *= c;
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -415,30 +420,70 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
         ps = 0.0f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pv[e] = exp2_fast(__builtin_fmaf(sv[e], c, -mu));
+          pv[e] = exp2_fast(__builtin_fmaf(sv[j][e], c, -mu));
           ps += pv[e];
         }
       }
+      bf16x8 pop;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pop[j][e] = static_cast<__bf16>(pv[e]);
+      for (int e = 0; e < 8; ++e) pop[e] = static_cast<__bf16>(pv[e]);
       l[j] += ps;
-    }
-    lds_wait(vr);
-    if (tb + kTileTokens > w.tok_hi) {
-      // positions past the range may hold anything: zero their V (0 * NaN
-      // would poison the accumulator)
+      return pop;
+    };
+    auto pv_tile = [&](int j, const bf16x8& pop) __attribute__((always_inline)) {
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const uint4 z = zero_past(make_uint4(vr[dt][0], vr[dt][1], vr[dt][2], vr[dt][3]), tb + 8 * g, w.tok_hi);
-        vr[dt] = u32x4{z.x, z.y, z.z, z.w};
+      for (int dt = 0; dt < 8; ++dt)
+        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[dt]), pop, o[j][dt], 0, 0, 0);
+    };
+    // Positions past the range may hold anything: zero their V (0 * NaN
+    // would poison the accumulator).
+    auto zero_past_range = [&]() __attribute__((always_inline)) {
+      if (tb + kTileTokens > w.tok_hi) {
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+          const uint4 z = zero_past(make_uint4(vr[dt][0], vr[dt][1], vr[dt][2], vr[dt][3]), tb + 8 * g, w.tok_hi);
+          vr[dt] = u32x4{z.x, z.y, z.z, z.w};
+        }
       }
+    };
+    if constexpr (NW == 8) {
+      // One workgroup per compute unit, the multi-row (prefill, long verify)
+      // shapes: the P.V of tile j - 1 is issued before the softmax of tile j,
+      // so the matrix cores work on one tile while the vector ALUs take the
+      // exponentials of the next.
+      // One branch masks all tiles, so the tiles' arithmetic below stays in
+      // one basic block.
+      if (edge) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) mask_tile(j);
+      }
+      bf16x8 pop = softmax_tile(0);
+      lds_wait(vr);
+      zero_past_range();
+#pragma unroll
+      for (int j = 1; j < NT; ++j) {
+        pv_tile(j - 1, pop);
+        pop = softmax_tile(j);
+      }
+      pv_tile(NT - 1, pop);
+    } else {
+      // Two workgroups per compute unit: the other workgroup's waves fill the
+      // matrix cores; all softmaxes first, then the P.V products.
+      bf16x8 pop[NT];
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (edge) mask_tile(j);
+        pop[j] = softmax_tile(j);
+      }
+      lds_wait(vr);
+      zero_past_range();
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[dt]), pop[j], o[j][dt], 0,
+                                                             0, 0);
     }
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[dt]), pop[j], o[j][dt], 0,
-                                                           0, 0);
   };
 
   // Everything loaded so far (query rows) completes before the ring starts,

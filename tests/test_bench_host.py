@@ -27,3 +27,36 @@ def test_traffic_figures_belong_to_the_profiled_workload():
     # never apply to another workload
     assert t["bytes_per_launch"] >= t["algorithmic_bytes_per_launch"]
     assert b.measured_traffic("qwen3-32b-decode") is None
+
+
+def _bench_module():
+    sys.path.insert(0, ROOT)
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    b = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(b)
+    return b
+
+
+def test_attention_flops_count_every_visible_position():
+    from paper_2607_03333_amd import synth
+    b = _bench_module()
+    for wl in (synth.make(synth.config_index("tiny-fork-f32")),
+               synth.make(synth.config_index("qwen3-32b-verify"), sessions=2, prefix=40, vocab=256)):
+        for i, st in enumerate(wl.steps):
+            # brute force: row j of a thread with n positions and r rows sees
+            # the positions 0 .. n - r + j
+            visible = 0
+            for seq, r in zip(st.seqs, st.n_rows):
+                n = wl.thread_len(seq, i)
+                for j in range(r):
+                    visible += sum(1 for p in range(n) if p <= n - r + j)
+            assert b.attention_flops(wl, i, st) == visible * wl.hq * 4 * wl.d
+            assert visible > 0
+
+
+def test_mfma_ridge_points():
+    b = _bench_module()
+    # bf16: 2.5 PFLOP/s over 8 TB/s; fp32 MFMA: 157.3 TFLOP/s over 8 TB/s
+    assert abs(b.MFMA_PEAK_TFLOPS["bf16"] * 1e12 / (b.HBM_PEAK_GBPS * 1e9) - 312.5) < 1e-9
+    assert abs(b.MFMA_PEAK_TFLOPS["f32"] * 1e12 / (b.HBM_PEAK_GBPS * 1e9) - 19.6625) < 1e-9
