@@ -403,6 +403,16 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
           ps += pv[e];
         }
       }
+      if constexpr (NW == 8) {
+        // Scheduling hint for the block that holds the previous tile's P.V:
+        // alternate one MFMA with three vector instructions of this tile's
+        // exponentials instead of issuing the MFMAs back to back.
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
+        }
+      }
       if (__ballot(!(ps <= kRescaleSum) || m[j] == kNegInf) != 0) {
         float mx = fmaxf(fmaxf(fmaxf(sv[j][0], sv[j][1]), fmaxf(sv[j][2], sv[j][3])),
                          fmaxf(fmaxf(sv[j][4], sv[j][5]), fmaxf(sv[j][6], sv[j][7])));
