@@ -313,7 +313,26 @@ int spork_ngram_propose(const int32_t* tokens, const int64_t* seq_off, int32_t n
 #define SPORK_KERNEL_CONF_FINAL 5  /* confidence: per-row log-probability and per-probe gate */
 #define SPORK_KERNEL_NGRAM_SCAN 6  /* n-gram drafts: per-chunk longest latest key match */
 #define SPORK_KERNEL_NGRAM_DRAFTS 7 /* n-gram drafts: per-sequence choice and draft copy */
-#define SPORK_KERNEL_KINDS 8
+#define SPORK_KERNEL_READ_CEILING 8 /* streaming-read ceiling (measurement aid) */
+#define SPORK_KERNEL_KINDS 9
+
+/* Streaming-read ceiling (a measurement aid, not a step of the method): read
+ * `bytes` of the device buffer `src` once, with `grid` workgroups of 256
+ * threads, each taking a contiguous share. It gives the bandwidth a plain
+ * read stream reaches on this device, the ceiling the attention launch is
+ * compared with.
+ *   mode 0: 16-byte register loads, 8 in flight per thread;
+ *   mode 1: direct-to-LDS loads in the bf16 attention kernel's ring shape
+ *           (4 waves, 4 slots of 16 KB, 3 in flight) with no arithmetic;
+ *           bytes must be a multiple of grid * 16384;
+ *   mode 2: as mode 0 with non-temporal loads;
+ *   mode 3: as mode 1 with non-temporal loads (same bytes rule).
+ * sink (device, caller-owned): grid * 256 uint32 words, overwritten with
+ * XOR folds of the data (so no load is dead). src 16-byte aligned, bytes a
+ * positive multiple of 16, 1 <= grid <= 65536; otherwise SPORK_E_INVAL and
+ * nothing is launched. One launch on `stream`. */
+int spork_read_ceiling(const void* src, int64_t bytes, int32_t grid, int32_t mode, uint32_t* sink,
+                       hipStream_t stream);
 
 /* While enabled (per calling thread), every hot-path call records a HIP event
  * before and after each of its kernels on the caller's stream. */

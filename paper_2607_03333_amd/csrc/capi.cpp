@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "block_manager.h"
+#include "ceiling_kernels.h"
 #include "kernels.h"
 #include "ngram_kernels.h"
 #include "vocab_kernels.h"
@@ -553,6 +554,20 @@ int spork_ngram_propose(const int32_t* tokens, const int64_t* seq_off, int32_t n
     if (rc != SPORK_OK) return rc;
     return hip_status(timed(SPORK_KERNEL_NGRAM_DRAFTS, stream, [&] { return spork::launch_ngram_drafts(a, stream); }),
                       "spork_ngram_propose (drafts)");
+  });
+}
+
+int spork_read_ceiling(const void* src, int64_t bytes, int32_t grid, int32_t mode, uint32_t* sink,
+                       hipStream_t stream) {
+  return guarded([&] {
+    if (src == nullptr || sink == nullptr) return fail(SPORK_E_INVAL, "NULL pointer");
+    if (!aligned16(src) || bytes <= 0 || bytes % 16 != 0) return fail(SPORK_E_INVAL, "src 16-byte aligned, bytes a positive multiple of 16");
+    if (grid < 1 || grid > 65536 || mode < 0 || mode > 3) return fail(SPORK_E_INVAL, "1 <= grid <= 65536 and mode 0 to 3");
+    if ((mode == 1 || mode == 3) && bytes % (static_cast<int64_t>(grid) * 16384) != 0)
+      return fail(SPORK_E_INVAL, "mode 1: bytes must be a multiple of grid * 16384");
+    return hip_status(timed(SPORK_KERNEL_READ_CEILING, stream,
+                            [&] { return spork::launch_read_ceiling(src, bytes, grid, mode, sink, stream); }),
+                      "spork_read_ceiling");
   });
 }
 

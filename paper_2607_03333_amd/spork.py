@@ -31,9 +31,10 @@ SPORK_KERNEL_CONF_CHUNKS = 4
 SPORK_KERNEL_CONF_FINAL = 5
 SPORK_KERNEL_NGRAM_SCAN = 6
 SPORK_KERNEL_NGRAM_DRAFTS = 7
-SPORK_KERNEL_KINDS = 8
+SPORK_KERNEL_READ_CEILING = 8
+SPORK_KERNEL_KINDS = 9
 KERNEL_NAMES = ("attn_partial", "merge", "argmax", "accept", "conf_chunks", "conf_final", "ngram_scan",
-                "ngram_drafts")
+                "ngram_drafts", "read_ceiling")
 
 _c_i32 = ctypes.c_int32
 _c_i64 = ctypes.c_int64
@@ -97,6 +98,7 @@ _SIGNATURES = {
     "spork_ngram_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
     "spork_ngram_propose": (ctypes.c_int, [_p, _p, _c_i32, _c_i64, _c_i32, _c_i32, _c_i32, _p, _p, _p,
                                            ctypes.c_size_t, _p]),
+    "spork_read_ceiling": (ctypes.c_int, [_p, _c_i64, _c_i32, _c_i32, _p, _p]),
     "spork_timing_enable": (ctypes.c_int, [_c_i32]),
     "spork_timing_read": (ctypes.c_int, [_p, _p]),
 }
@@ -320,6 +322,11 @@ def spork_ngram_propose(tokens, seq_off, n_seqs, max_len, n_min, n_max, k, draft
     _check(lib().spork_ngram_propose(_ptr(tokens), _ptr(seq_off), n_seqs, max_len, n_min, n_max, k,
                                      _ptr(drafts), _ptr(n_drafts), _ptr(workspace), ws_bytes,
                                      _stream(stream)))
+
+
+# ---- measurement aid --------------------------------------------------------
+def spork_read_ceiling(src, nbytes, grid, mode, sink, stream=None):
+    _check(lib().spork_read_ceiling(_ptr(src), nbytes, grid, mode, _ptr(sink), _stream(stream)))
 
 
 # ---- kernel timing ------------------------------------------------------------

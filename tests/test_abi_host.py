@@ -195,6 +195,20 @@ def test_ngram_error_codes():
     ng(None, None, 0, 0, 1, 3, 4, None, None, None, stream=0)   # nothing to do
 
 
+def test_read_ceiling_error_codes():
+    """The read-ceiling aid rejects bad arguments before any launch."""
+    rc = spork.spork_read_ceiling
+    for src, nbytes, grid, mode in ((None, 1 << 20, 4, 0), (256, 0, 4, 0), (256, 24, 4, 0), (264, 1 << 20, 4, 0),
+                                    (256, 1 << 20, 0, 0), (256, 1 << 20, 65537, 0), (256, 1 << 20, 4, 4),
+                                    (256, 1 << 20, 4, -1), (256, 3 * 16384, 2, 1), (256, 3 * 16384, 2, 3)):
+        with pytest.raises(spork.SporkError) as e:
+            rc(src, nbytes, grid, mode, 256, stream=0)
+        assert e.value.code == spork.SPORK_E_INVAL
+    with pytest.raises(spork.SporkError) as e:
+        rc(256, 1 << 20, 4, 0, None, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL
+
+
 def _plan_for(wl, groups=None, n_cu=256):
     c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
     for stp in wl.steps:
