@@ -177,6 +177,8 @@ typedef struct spork_plan_info {
   int32_t attn_waves;      /* waves per attention workgroup (bf16: 4, two workgroups per
                               compute unit, or 8 when a range has more than 16 row tiles,
                               one per compute unit; fp32: 1) */
+  size_t control_bytes;    /* leading workspace bytes that hold control words (see
+                              spork_workspace_clear) */
 } spork_plan_info;
 
 /* Plan one step for n_threads threads.
@@ -200,15 +202,29 @@ int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap);
  *  Hot path.
  * ======================================================================== */
 
+/* Workspace control words. The first info.control_bytes bytes of a plan's
+ * workspace are the work-list cursors of the persistent bf16 attention
+ * launch. They must be zero when a call starts, and every call leaves them
+ * zero (its last launch clears them). Zero them once after allocating a workspace, and again
+ * before a workspace serves a plan with a larger control_bytes than the
+ * plans it served before (bytes past the old control words held partial
+ * results): this call does it with one small kernel on `stream` (no
+ * memset, so it may be captured in a HIP graph). ws_bytes >=
+ * info.control_bytes; the rest of the workspace is not touched. */
+int spork_workspace_clear(const spork_plan* plan, void* workspace, size_t ws_bytes,
+                          hipStream_t stream);
+
 /* Batched decode attention of main and probe rows (Sections 4.1 and 4.3).
  * q (device [rows][Hq][D] dtype); k_cache, v_cache (device pools);
  * out (device [rows][Hq][D] dtype); lse (device [rows][Hq] float32, nullable);
- * workspace (device, ws_bytes >= info.workspace_bytes, any contents on
- * entry; it holds the partial results and the attention's list cursors, so
- * calls that share a workspace must not overlap).
- * Kernels, in order on `stream`: a small kernel that zeroes the list cursors
- * (bf16), the cascade partial attention over prefix and suffix ranges, the
- * log-sum-exp merge. */
+ * workspace (device, 256-byte aligned, ws_bytes >= info.workspace_bytes;
+ * control words zero on entry, see spork_workspace_clear, the rest any
+ * contents; it holds the partial results and the counters, so calls that
+ * share a workspace must not overlap).
+ * Two launches on `stream`: the partial attention over prefix and suffix
+ * ranges (bf16: persistent workgroups working through per-compute-unit
+ * lists), then the log-sum-exp merge, which also returns the cursors to
+ * zero. */
 int spork_attn_decode(const spork_plan* plan, const void* dev_image, const void* q,
                       const void* k_cache, const void* v_cache, void* out, float* lse,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
@@ -229,12 +245,14 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
  * Ties pick the lowest vocabulary index; logits must be finite. A draft of
  * -1 (padding after fewer than k_drafts real drafts) never matches.
  * workspace: the attention's workspace followed (at a 256-byte aligned
- * offset) by spork_verify_workspace_bytes; ws_bytes covers both.
- * With a plan the step is three launches on `stream`. bf16: a kernel that
- * zeroes the attention's cursors, the partial attention whose workgroups
- * take the argmax units once their own lists are done, then the merge
- * together with the accept. fp32: the argmax, the partial attention, the
- * merge with the accept. */
+ * offset) by spork_verify_workspace_bytes; ws_bytes covers both. With a
+ * plan the workspace's control words must be zero on entry
+ * (spork_workspace_clear).
+ * With a bf16 plan the step is two launches on `stream`: the partial
+ * attention, whose persistent workgroups take the argmax units once their
+ * own lists are done, then the merge together with the accept (and the
+ * cursor clear). fp32 plan: the argmax, the partial attention, the merge
+ * with the accept. Without a plan: the argmax, then the accept. */
 int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q,
                         const void* k_cache, const void* v_cache, void* out, float* lse,
                         const void* logits, int32_t logits_dtype, int32_t vocab,

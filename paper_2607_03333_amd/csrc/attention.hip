@@ -202,7 +202,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
   __syncthreads();
   const int taken = __builtin_amdgcn_readfirstlane(next_unit);
-  if (taken >= list_len) break;
+  if (taken < 0 || taken >= list_len) break;
   const WaveDesc w = a.waves[list0 + taken];
   if (w.item < 0) {  // padding (not emitted on persistent lists): every wave reads next_unit first
     __syncthreads();
@@ -556,7 +556,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
       if (tid == 0) next_unit = atomicAdd(a.cursors + a.n_lists, 1);
       __syncthreads();
       const int u = __builtin_amdgcn_readfirstlane(next_unit);
-      if (u >= a.tail_units) break;
+      if (u < 0 || u >= a.tail_units) break;
       const int row = u / a.acc.chunks, c = u % a.acc.chunks;
       uint64_t* key = a.acc.keys + static_cast<size_t>(row) * a.acc.chunks + c;
       const size_t roff = static_cast<size_t>(row) * a.acc.vocab;
@@ -782,6 +782,10 @@ __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bo
 template <int D, typename OutT>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int PER = D / 64;
+  // The attention launch is done with its cursors: return them to zero for
+  // the workspace's next call.
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < a.n_cursors; i += 256) a.cursors[i] = 0;
   const int merge_blocks = (a.n_out + 3) / 4;
   if (static_cast<int>(blockIdx.x) >= merge_blocks) {
     // fused accept: one verify thread per wave
@@ -875,8 +879,9 @@ hipError_t launch_counter_reset(int32_t* counters, int32_t n, hipStream_t stream
 }
 
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
-  const int blocks = (a.n_out + 3) / 4 + (a.acc.n_verify + 3) / 4;
-  if (blocks == 0) return hipSuccess;
+  int blocks = (a.n_out + 3) / 4 + (a.acc.n_verify + 3) / 4;
+  if (blocks == 0 && a.n_cursors == 0) return hipSuccess;
+  if (blocks == 0) blocks = 1;  // only the cursors to clear
   if (a.dtype == 1 && a.head_dim == 128)
     hipLaunchKernelGGL((merge_kernel<128, __bf16>), dim3(blocks), dim3(256), 0, stream, a);
   else if (a.dtype == 0 && a.head_dim == 128)

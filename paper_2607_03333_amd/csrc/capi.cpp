@@ -36,7 +36,7 @@ int fail(int code, const std::string& msg) {
   return code;
 }
 
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 
 // Per-thread kernel timing: event pairs recorded around each launch.
 struct Timing {
@@ -320,6 +320,7 @@ int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info) {
   const int64_t per_tok = 2LL * p.shape.hkv * p.shape.head_dim * p.shape.elem_bytes;
   info->unique_kv_bytes = (p.shared_tokens + p.private_tokens) * per_tok;
   info->flat_kv_bytes = p.flat_tokens * per_tok;
+  info->control_bytes = p.control_bytes;
   return SPORK_OK;
 }
 
@@ -330,8 +331,22 @@ int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap) {
   return SPORK_OK;
 }
 
-// Attention over a plan; with `acc` (a verify step) the argmax runs first and
-// the accept rides in the merge launch.
+int spork_workspace_clear(const spork_plan* plan, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  return guarded([&] {
+    if (plan == nullptr) return fail(SPORK_E_INVAL, "plan is NULL");
+    const size_t n = plan->p.control_bytes;
+    if (n == 0) return SPORK_OK;
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+      return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
+    if (ws_bytes < n) return fail(SPORK_E_CAPACITY, "workspace smaller than info.control_bytes");
+    return hip_status(spork::launch_counter_reset(static_cast<int32_t*>(workspace), static_cast<int32_t>(n / 4), stream),
+                      "spork_workspace_clear");
+  });
+}
+
+// Attention over a plan. bf16 (persistent): the attention launch (with the
+// argmax units of a verify step in its tail), then the merge launch (with
+// the accept). fp32: the argmax first (verify), the attention, the merge.
 static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
                      const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
                      const spork::AcceptArgs* acc, hipStream_t stream) {
@@ -374,19 +389,21 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.v_cache = v_cache;
   a.out = out;
   a.lse = lse;
-  a.part_o = static_cast<float*>(workspace);
-  a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + p.off_ws_ml);
-  // The persistent bf16 kernel needs its cursors at zero (a small kernel
-  // clears them); in a verify step it also runs the argmax units after its
-  // lists, and the accept rides in the merge launch. The fp32 kernel is not
-  // persistent: there the argmax has a launch of its own first.
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.part_o = reinterpret_cast<float*>(ws + p.off_ws_o);
+  a.part_ml = reinterpret_cast<float*>(ws + p.off_ws_ml);
+  a.n_cursors = p.n_cursors;
+  // The persistent bf16 kernel takes its units through cursors that are zero
+  // on entry (the merge launch clears them again); in a verify step it also
+  // runs the argmax units after its lists, and the accept rides in the merge
+  // launch: two launches. The fp32 kernel is not persistent: the argmax has
+  // a launch of its own first.
   const bool persistent = p.shape.persistent;
   const bool verify = acc != nullptr && acc->n_verify > 0;
   int rc = SPORK_OK;
   if (verify) a.acc = *acc;
   if (persistent) {
     if (verify) a.tail_units = acc->n_verify * (acc->k_drafts + 1) * acc->chunks;
-    rc = hip_status(spork::launch_counter_reset(a.cursors, p.n_lists + 1, stream), "spork_attn_decode (cursor reset)");
   } else if (verify) {
     rc = hip_status(timed(SPORK_KERNEL_ARGMAX, stream, [&] { return spork::launch_argmax(a.acc, stream); }),
                     "spork_verify_accept (argmax)");

@@ -54,12 +54,15 @@ struct AttnArgs {
   // through after its lists, through cursors[n_lists]; 0 when the argmax has
   // a launch of its own.
   int32_t tail_units;
+  // Cursors the merge launch returns to zero for the next call (the
+  // persistent launch's n_lists + 1; 0 otherwise).
+  int32_t n_cursors;
 };
 
 // true if a kernel exists for this (dtype, head_dim, block_size, row_tiles)
 bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles, int32_t waves);
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream);
-// zero n int32 counters (the list cursors, before a persistent attention launch)
+// zero n int32 words (a workspace's control words)
 hipError_t launch_counter_reset(int32_t* counters, int32_t n, hipStream_t stream);
 // log-sum-exp merge (+ accept of a.acc.n_verify verify threads)
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);

@@ -429,11 +429,15 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   put(p.off_part_slot, part_slot.data(), part_slot.size() * sizeof(int32_t));
   put(p.off_wg_off, wg_off.data(), wg_off.size() * sizeof(int32_t));
 
-  const size_t o_bytes = align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
-  p.off_ws_ml = o_bytes;
-  p.off_ws_cursors = o_bytes + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
-  // list cursors, then the cursor of the argmax units a verify launch takes after its lists
-  p.workspace_bytes = p.off_ws_cursors + align256(static_cast<size_t>(p.n_lists + 1) * sizeof(int32_t));
+  // Control words: the list cursors and the cursor of the argmax units a
+  // verify launch takes after its lists (persistent launches); then the
+  // partial outputs and their (m, l) pairs.
+  p.off_ws_cursors = 0;
+  p.n_cursors = shape.persistent ? p.n_lists + 1 : 0;
+  p.control_bytes = align256(static_cast<size_t>(p.n_cursors) * sizeof(int32_t));
+  p.off_ws_o = p.control_bytes;
+  p.off_ws_ml = p.off_ws_o + align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
+  p.workspace_bytes = p.off_ws_ml + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
   *out = std::move(p);
   return "";
 }

@@ -39,9 +39,14 @@ struct Plan {
   std::vector<uint8_t> image;
   size_t off_waves = 0, off_items = 0, off_rows = 0, off_tables = 0, off_merge_off = 0,
          off_part_slot = 0, off_wg_off = 0;
-  size_t workspace_bytes = 0;  // partial outputs + (m, l) pairs + list cursors
-  size_t off_ws_ml = 0;        // byte offset of the (m, l) pairs in the workspace
-  size_t off_ws_cursors = 0;   // byte offset of the list cursors (zeroed before each launch)
+  // Workspace: control words first (zero between calls: the list cursors of
+  // a persistent launch), then the partial outputs and their (m, l) pairs.
+  size_t workspace_bytes = 0;
+  size_t control_bytes = 0;
+  int32_t n_cursors = 0;       // n_lists + 1 for a persistent launch, else 0
+  size_t off_ws_cursors = 0;   // byte offsets inside the workspace
+  size_t off_ws_o = 0;
+  size_t off_ws_ml = 0;
 };
 
 // Returns "" on success, else an error message (nothing is built).

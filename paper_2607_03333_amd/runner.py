@@ -56,13 +56,17 @@ class Step:
             self.next_token = torch.full((self.n_verify,), -1, dtype=torch.int32, device=dev)
             self.argmax = torch.full((self.n_verify * (st.verify_k + 1),), -1, dtype=torch.int32, device=dev)
         self.workspace = torch.empty(max(att_ws + acc_ws, 256), dtype=torch.uint8, device=dev)
+        spork.spork_workspace_clear(self.plan, self.workspace)
         self.dw = dw
 
     def poison(self):
-        """Fill outputs and workspace with NaN / -1 so unwritten values show."""
+        """Fill outputs and workspace with NaN / -1 so unwritten values show
+        (the workspace's control words are then zeroed again, as a call
+        requires)."""
         self.out.fill_(float("nan"))
         self.lse.fill_(float("nan"))
         self.workspace.fill_(0xFF)
+        spork.spork_workspace_clear(self.plan, self.workspace)
         if self.verify:
             self.accept_len.fill_(-1)
             self.next_token.fill_(-1)

@@ -60,7 +60,8 @@ class spork_plan_info(ctypes.Structure):
                 ("max_row_tiles", _c_i32), ("attn_grid", _c_i32),
                 ("image_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
                 ("shared_tokens", _c_i64), ("private_tokens", _c_i64),
-                ("unique_kv_bytes", _c_i64), ("flat_kv_bytes", _c_i64), ("attn_waves", _c_i32)]
+                ("unique_kv_bytes", _c_i64), ("flat_kv_bytes", _c_i64), ("attn_waves", _c_i32),
+                ("control_bytes", ctypes.c_size_t)]
 
 
 # name -> (restype, argtypes); every name is declared in include/spork.h
@@ -86,6 +87,7 @@ _SIGNATURES = {
     "spork_plan_destroy": (ctypes.c_int, [_p]),
     "spork_plan_get_info": (ctypes.c_int, [_p, ctypes.POINTER(spork_plan_info)]),
     "spork_plan_image": (ctypes.c_int, [_p, _p, ctypes.c_size_t]),
+    "spork_workspace_clear": (ctypes.c_int, [_p, _p, ctypes.c_size_t, _p]),
     "spork_attn_decode": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "spork_verify_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i32, _c_i32,
                                                     ctypes.POINTER(ctypes.c_size_t)]),
@@ -272,6 +274,11 @@ def spork_plan_image(plan):
 
 
 # ---- hot path ---------------------------------------------------------------
+def spork_workspace_clear(plan, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spork_workspace_clear(plan, _ptr(workspace), ws_bytes, _stream(stream)))
+
+
 def spork_attn_decode(plan, dev_image, q, k_cache, v_cache, out, lse, workspace, stream=None):
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().spork_attn_decode(plan, _ptr(dev_image), _ptr(q), _ptr(k_cache), _ptr(v_cache),

@@ -126,6 +126,21 @@ class Step:
     verify_k: int = 0
 
 
+def draw_kv(seed, n, hkv, d, dtype):
+    """K then V of ``n`` tokens from the stream ``default_rng(seed)``, storage dtype."""
+    r = np.random.default_rng(seed)
+    k = to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype)
+    v = to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype)
+    return k, v
+
+
+def _draw_segments(segs, hkv, d, dtype):
+    pairs = [draw_kv(seed, n, hkv, d, dtype) for seed, n in segs]
+    if len(pairs) == 1:
+        return pairs[0]
+    return np.concatenate([p[0] for p in pairs]), np.concatenate([p[1] for p in pairs])
+
+
 @dataclass
 class Workload:
     index: int
@@ -146,9 +161,31 @@ class Workload:
     suffix_k: dict                      # per seq [suffix + drafts, Hkv, D]
     suffix_v: dict
     steps: list = field(default_factory=list)
+    # Where every K/V array comes from: ("p", session) and ("s", seq) map to
+    # segments (seed, tokens), each drawn K then V from default_rng(seed).
+    # Without stored arrays (built with kv=False) they are drawn on demand.
+    kv_src: dict = field(default_factory=dict)
+    _kv_cache: dict = field(default_factory=dict, repr=False)
 
     def thread(self, seq):
         return next(t for t in self.threads if t.seq == seq)
+
+    def _lazy(self, key):
+        if key not in self._kv_cache:
+            if len(self._kv_cache) >= 8:
+                self._kv_cache.pop(next(iter(self._kv_cache)))
+            self._kv_cache[key] = _draw_segments(self.kv_src[key], self.hkv, self.d, self.dtype)
+        return self._kv_cache[key]
+
+    def prefix_kv(self, session):
+        if self.prefix_k is not None:
+            return self.prefix_k[session], self.prefix_v[session]
+        return self._lazy(("p", session))
+
+    def suffix_kv(self, seq):
+        if self.suffix_k is not None:
+            return self.suffix_k[seq], self.suffix_v[seq]
+        return self._lazy(("s", seq))
 
     def context(self, seq, length=None):
         """Logical K, V of a thread, storage dtype: a root's session prefix, or
@@ -157,9 +194,10 @@ class Workload:
         if t.parent >= 0:
             pk, pv = self.context(t.parent, t.fork_len)
         else:
-            pk, pv = self.prefix_k[t.session], self.prefix_v[t.session]
-        k = np.concatenate([pk, self.suffix_k[seq]])
-        v = np.concatenate([pv, self.suffix_v[seq]])
+            pk, pv = self.prefix_kv(t.session)
+        sk, sv = self.suffix_kv(seq)
+        k = np.concatenate([pk, sk])
+        v = np.concatenate([pv, sv])
         if length is not None:
             k, v = k[:length], v[:length]
         return k, v
@@ -210,6 +248,19 @@ class Workload:
         return total * per_tok
 
 
+def _draw_all(kv_src, prefix_keys, seqs, hkv, d, dtype, kv):
+    """Stored K/V arrays of a workload (prefixes by session, suffixes by
+    sequence), drawn in parallel; all None when ``kv`` is false."""
+    if not kv:
+        return None, None, None, None
+    keys = list(prefix_keys) + [("s", q) for q in seqs]
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        pairs = list(ex.map(lambda key: _draw_segments(kv_src[key], hkv, d, dtype), keys))
+    n_p = len(prefix_keys)
+    return ([p[0] for p in pairs[:n_p]], [p[1] for p in pairs[:n_p]],
+            {q: pairs[n_p + i][0] for i, q in enumerate(seqs)}, {q: pairs[n_p + i][1] for i, q in enumerate(seqs)})
+
+
 def _draw_suffix(rng, spec, n):
     kind = spec[0]
     if kind == "fixed":
@@ -225,11 +276,13 @@ def _draw_suffix(rng, spec, n):
 
 
 def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=None,
-         block_size=None, q_gain=1.0, tie_prob=TIE_PROB):
+         block_size=None, q_gain=1.0, tie_prob=TIE_PROB, kv=True):
     """Build workload ``index`` (0..4), optionally shrunk for fast tests.
 
     Overrides keep the workload's structure (forks, rows, GQA, dtype) while
-    changing its size. ``q_gain`` multiplies Q (a sharper softmax).
+    changing its size. ``q_gain`` multiplies Q (a sharper softmax). With
+    ``kv=False`` no K/V array is drawn up front; ``context`` draws a
+    thread's from its own seed streams when asked (same values).
     """
     index = config_index(index)
     cfg = dict(CONFIGS[index])
@@ -283,19 +336,10 @@ def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=No
     def normal(shape, r=rng):
         return r.standard_normal(shape, dtype=np.float32)
 
-    def kv_pair(key, n):
-        r = np.random.default_rng([42, index] + list(key))
-        return (to_storage(normal((n, hkv, d), r), dtype),
-                to_storage(normal((n, hkv, d), r), dtype))
-
-    jobs = [((1, s), plen) for s in range(n_sess)]
-    jobs += [((2, t.seq), t.suffix + t.drafts) for t in ordered]
-    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
-        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
-    prefix_k = [pairs[s][0] for s in range(n_sess)]
-    prefix_v = [pairs[s][1] for s in range(n_sess)]
-    suffix_k = {t.seq: pairs[n_sess + i][0] for i, t in enumerate(ordered)}
-    suffix_v = {t.seq: pairs[n_sess + i][1] for i, t in enumerate(ordered)}
+    kv_src = {("p", s_): [([42, index, 1, s_], plen)] for s_ in range(n_sess)}
+    kv_src.update({("s", t.seq): [([42, index, 2, t.seq], t.suffix + t.drafts)] for t in ordered})
+    prefix_k, prefix_v, suffix_k, suffix_v = _draw_all(kv_src, [("p", s_) for s_ in range(n_sess)],
+                                                       [t.seq for t in ordered], hkv, d, dtype, kv)
 
     build_ops = [("new", t.seq) for t in threads if t.role == "main"]
     build_ops += [("append", t.seq, plen) for t in threads if t.role == "main"]
@@ -307,7 +351,7 @@ def make(index, sessions=None, prefix=None, suffix=None, vocab=None, verify_k=No
                   dtype=dtype, logits_dtype=cfg["logits_dtype"], sm_scale=sm_scale,
                   num_blocks=num_blocks, free_order=free_order, threads=threads,
                   prefix_len=[plen] * n_sess, prefix_k=prefix_k, prefix_v=prefix_v,
-                  suffix_k=suffix_k, suffix_v=suffix_v)
+                  suffix_k=suffix_k, suffix_v=suffix_v, kv_src=kv_src)
 
     def q_for(n_rows_total):
         return to_storage(normal((n_rows_total, hq, d)) * np.float32(q_gain), dtype)
@@ -413,7 +457,7 @@ TREE_NAME = "qwen3-30b-a3b-staggered"
 
 
 def make_tree(sessions=32, prefix=32768, probes=4, stride=200, probe_tokens=(8, 64), main_extra=(1, 200),
-              hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0):
+              hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0, kv=True):
     """Staggered probes (Algorithm 1's retry loop): a decode step over a
     prefix tree of forks.
 
@@ -458,16 +502,10 @@ def make_tree(sessions=32, prefix=32768, probes=4, stride=200, probe_tokens=(8, 
     def normal(shape, r=rng):
         return r.standard_normal(shape, dtype=np.float32)
 
-    def kv_pair(key, n):
-        r = np.random.default_rng([42, index] + list(key))
-        return (to_storage(normal((n, hkv, d), r), dtype),
-                to_storage(normal((n, hkv, d), r), dtype))
-
-    jobs = [((1, s), prefix) for s in range(sessions)] + [((2, t.seq), t.suffix) for t in ordered]
-    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
-        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
-    suffix_k = {t.seq: pairs[sessions + i][0] for i, t in enumerate(ordered)}
-    suffix_v = {t.seq: pairs[sessions + i][1] for i, t in enumerate(ordered)}
+    kv_src = {("p", s_): [([42, index, 1, s_], prefix)] for s_ in range(sessions)}
+    kv_src.update({("s", t.seq): [([42, index, 2, t.seq], t.suffix)] for t in ordered})
+    prefix_k, prefix_v, suffix_k, suffix_v = _draw_all(kv_src, [("p", s_) for s_ in range(sessions)],
+                                                       [t.seq for t in ordered], hkv, d, dtype, kv)
 
     ops = []
     for s in range(sessions):
@@ -489,8 +527,8 @@ def make_tree(sessions=32, prefix=32768, probes=4, stride=200, probe_tokens=(8, 
     wl = Workload(index=index, name=TREE_NAME, hq=hq, hkv=hkv, d=d, block_size=bs, dtype=dtype,
                   logits_dtype=dtype, sm_scale=float(np.float32(1.0 / math.sqrt(d))),
                   num_blocks=num_blocks, free_order=free_order, threads=threads,
-                  prefix_len=[prefix] * sessions, prefix_k=[pairs[s][0] for s in range(sessions)],
-                  prefix_v=[pairs[s][1] for s in range(sessions)], suffix_k=suffix_k, suffix_v=suffix_v)
+                  prefix_len=[prefix] * sessions, prefix_k=prefix_k, prefix_v=prefix_v,
+                  suffix_k=suffix_k, suffix_v=suffix_v, kv_src=kv_src)
     q = to_storage(normal((len(ordered), hq, d)) * np.float32(q_gain), dtype)
     wl.steps.append(Step(seqs=[t.seq for t in ordered], n_rows=[1] * len(ordered),
                          groups=[t.session for t in ordered], q=q, ops_before=ops))
@@ -501,7 +539,7 @@ PREFILL_NAME = "qwen3-30b-a3b-probe-prefill"
 
 
 def make_prefill(sessions=64, prefix=32768, probes=2, cot=("loguniform", 1, 4096), opener=(8, 50),
-                 hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0):
+                 hq=32, hkv=4, d=128, block_size=16, dtype=BF16, q_gain=1.0, kv=True):
     """Probe prefill over the shared prefix (Section 4.1: the probe's prefill
     is a prefix-cache hit): one step in which every main thread decodes one
     row while its probes, just forked after the chain of thought observed so
@@ -540,16 +578,10 @@ def make_prefill(sessions=64, prefix=32768, probes=2, cot=("loguniform", 1, 4096
     def normal(shape, r=rng):
         return r.standard_normal(shape, dtype=np.float32)
 
-    def kv_pair(key, n):
-        r = np.random.default_rng([42, index] + list(key))
-        return (to_storage(normal((n, hkv, d), r), dtype),
-                to_storage(normal((n, hkv, d), r), dtype))
-
-    jobs = [((1, s), prefix) for s in range(sessions)] + [((2, t.seq), t.suffix) for t in ordered]
-    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
-        pairs = list(ex.map(lambda j: kv_pair(*j), jobs))
-    suffix_k = {t.seq: pairs[sessions + i][0] for i, t in enumerate(ordered)}
-    suffix_v = {t.seq: pairs[sessions + i][1] for i, t in enumerate(ordered)}
+    kv_src = {("p", s_): [([42, index, 1, s_], prefix)] for s_ in range(sessions)}
+    kv_src.update({("s", t.seq): [([42, index, 2, t.seq], t.suffix)] for t in ordered})
+    prefix_k, prefix_v, suffix_k, suffix_v = _draw_all(kv_src, [("p", s_) for s_ in range(sessions)],
+                                                       [t.seq for t in ordered], hkv, d, dtype, kv)
 
     ops = []
     for s in range(sessions):
@@ -563,8 +595,8 @@ def make_prefill(sessions=64, prefix=32768, probes=2, cot=("loguniform", 1, 4096
     wl = Workload(index=index, name=PREFILL_NAME, hq=hq, hkv=hkv, d=d, block_size=bs, dtype=dtype,
                   logits_dtype=dtype, sm_scale=float(np.float32(1.0 / math.sqrt(d))),
                   num_blocks=num_blocks, free_order=free_order, threads=threads,
-                  prefix_len=[prefix] * sessions, prefix_k=[pairs[s][0] for s in range(sessions)],
-                  prefix_v=[pairs[s][1] for s in range(sessions)], suffix_k=suffix_k, suffix_v=suffix_v)
+                  prefix_len=[prefix] * sessions, prefix_k=prefix_k, prefix_v=prefix_v,
+                  suffix_k=suffix_k, suffix_v=suffix_v, kv_src=kv_src)
     rows = [1 if t.role == "main" else t.suffix for t in ordered]
     q = to_storage(normal((sum(rows), hq, d)) * np.float32(q_gain), dtype)
     wl.steps.append(Step(seqs=[t.seq for t in ordered], n_rows=rows, groups=[t.session for t in ordered],
@@ -631,9 +663,7 @@ def add_supersession_step(wl, more=(20, 120), own=(4, 30), seed=0):
     hkv, d, dtype = wl.hkv, wl.d, wl.dtype
 
     def kv(key, n):
-        r = np.random.default_rng([42, 9, seed, key])
-        return (to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype),
-                to_storage(r.standard_normal((n, hkv, d), dtype=np.float32), dtype))
+        return draw_kv([42, 9, seed, key], n, hkv, d, dtype)
 
     ops, seqs = [], []
     for m in [t for t in wl.threads if t.role == "main" and t.seq in prev.seqs]:
@@ -642,15 +672,20 @@ def add_supersession_step(wl, more=(20, 120), own=(4, 30), seed=0):
             ops.append(("free", live[0].seq))
         add = int(rng.integers(more[0], more[1] + 1))
         length = wl.thread_len(m.seq, si)
-        k, v = kv(m.seq, add)
-        wl.suffix_k[m.seq] = np.concatenate([wl.suffix_k[m.seq], k])
-        wl.suffix_v[m.seq] = np.concatenate([wl.suffix_v[m.seq], v])
+        wl.kv_src[("s", m.seq)] = wl.kv_src[("s", m.seq)] + [([42, 9, seed, m.seq], add)]
+        wl._kv_cache.pop(("s", m.seq), None)
+        if wl.suffix_k is not None:
+            k, v = kv(m.seq, add)
+            wl.suffix_k[m.seq] = np.concatenate([wl.suffix_k[m.seq], k])
+            wl.suffix_v[m.seq] = np.concatenate([wl.suffix_v[m.seq], v])
         m.suffix += add
         ops.append(("append", m.seq, add))
         n_own = int(rng.integers(own[0], own[1] + 1))
         t = Thread(seq=nid, session=m.session, role="probe", suffix=n_own, parent=m.seq, fork_len=length + add)
         wl.threads.append(t)
-        wl.suffix_k[nid], wl.suffix_v[nid] = kv(nid, n_own)
+        wl.kv_src[("s", nid)] = [([42, 9, seed, nid], n_own)]
+        if wl.suffix_k is not None:
+            wl.suffix_k[nid], wl.suffix_v[nid] = kv(nid, n_own)
         ops += [("fork", m.seq, nid), ("append", nid, n_own)]
         seqs += [m.seq] + [p.seq for p in live[1:]] + [nid]
         nid += 1

@@ -10,6 +10,7 @@ import pytest
 from hypothesis import given, settings, strategies as st
 
 import oracle
+import oracle_pool
 from paper_2607_03333_amd import spork, synth
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -28,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(spork._SIGNATURES)
-    assert spork.spork_version() == 1
+    assert spork.spork_version() == 2
 
 
 def _apply_both(ops, nb, bs, order):
@@ -250,70 +251,129 @@ def test_plan_unique_bytes_match_workload(index):
     spork.spork_cache_destroy(c)
 
 
-def _check_cover(wl, c, p):
-    """Decode the image: for every output (query row, head), the workgroups
-    that write one of its partials cover each visible position exactly once,
-    through block-table entries equal to the thread's own table."""
-    info, img = _decode_image(p)
+def _image_sections(info, img, n_out):
+    """Split a plan image into its sections (256-byte aligned, in order:
+    units, items, row descriptors, tables, merge offsets, partial slots,
+    unit lists)."""
     raw = img.view(np.int32)
-    # sections are 256-byte aligned in order: waves, items, rows, tables, merge_off, part_slot
-    nw = info["n_units"]
+    al = lambda nbytes: -(-nbytes // 256) * 256 // 4
+    nw, ni = info["n_units"], info["n_items"]
     waves = raw[: nw * 6].reshape(nw, 6)
-    off = -(-nw * 24 // 256) * 256 // 4
-    items = raw[off: off + info["n_items"] * 6].reshape(-1, 6)
-    off += -(-info["n_items"] * 24 // 256) * 256 // 4
-    nrow_desc = int(items[:, 4].sum())
-    rows = raw[off: off + 2 * nrow_desc].reshape(-1, 2)
-    off += -(-nrow_desc * 8 // 256) * 256 // 4
-    tables = raw[off:]
-    stp = wl.steps[-1]
-    row_seq = [s for s, n in zip(stp.seqs, stp.n_rows) for _ in range(n)]
+    off = al(nw * 24)
+    items = raw[off: off + ni * 6].reshape(-1, 6)
+    off += al(ni * 24)
+    nrow = int(items[:, 4].sum())
+    rows = raw[off: off + 2 * nrow].reshape(-1, 2)
+    off += al(nrow * 8)
+    n_part = info["n_partials"]
+    n_lists = info["attn_grid"] // 2 if info["attn_waves"] == 4 else info["attn_grid"]
+    o_wg = info["image_bytes"] // 4 - al(4 * (n_lists + 1))
+    o_ps = o_wg - al(4 * n_part)
+    o_mo = o_ps - al(4 * (n_out + 1))
+    return waves, items, rows, raw[off:o_mo], raw[o_mo: o_mo + n_out + 1], raw[o_ps: o_ps + n_part]
+
+
+def _check_cover(wl, c, p, step_index=-1):
+    """Decode the image: for every output (query row, head), the units that
+    write one of its partials cover each visible position exactly once,
+    through block-table entries equal to the thread's own table; every unit
+    row writes its partial inside its output's merge range and every merge
+    position is written once."""
+    info, img = _decode_image(p)
+    stp = wl.steps[step_index]
+    hq, bs = wl.hq, wl.block_size
+    n_out = sum(stp.n_rows) * hq
+    waves, items, rows, tables, merge_off, part_slot = _image_sections(info, img, n_out)
+    row_seq = np.repeat(np.asarray(stp.seqs), stp.n_rows)
     own = {s: spork.spork_block_table(c, s) for s in stp.seqs}
-    bs = wl.block_size
-    cover = {}
+    lens = {s: spork.spork_seq_len(c, s) for s in stp.seqs}
+    q_all, lo_all, top_all, slot_all = [], [], [], []
     for w in waves:
         item, lo, hi, row0, nr, part = (int(x) for x in w)
         if item < 0:
             continue
         it = items[item]
-        for i in range(nr):
-            qidx, hz = rows[it[3] + row0 + i]
-            top = min(hi, int(hz) + 1)
-            cover.setdefault(int(qidx), []).append((lo, top))
-            if top > lo:
-                seq = row_seq[int(qidx) // wl.hq]
-                blk = np.arange(lo // bs, (top - 1) // bs + 1)
-                assert np.all(blk < it[2])
-                assert np.array_equal(tables[it[1] + blk], own[seq][blk]), (seq, lo, top)
-    assert len(cover) == sum(stp.n_rows) * wl.hq
-    # the last three sections: merge offsets per output, the merge position
-    # of every unit row's partial, the unit lists
-    al = lambda n: -(-n * 4 // 256) * 256 // 4
-    n_out, n_part = sum(stp.n_rows) * wl.hq, info["n_partials"]
-    n_lists = info["attn_grid"] // 2 if info["attn_waves"] == 4 else info["attn_grid"]
-    o_wg = info["image_bytes"] // 4 - al(n_lists + 1)
-    o_ps = o_wg - al(n_part)
-    o_mo = o_ps - al(n_out + 1)
-    merge_off, part_slot = raw[o_mo: o_mo + n_out + 1], raw[o_ps: o_ps + n_part]
-    assert np.array_equal(np.sort(part_slot), np.arange(n_part))   # every position written once
-    for w in waves:
-        item, lo, hi, row0, nr, part = (int(x) for x in w)
-        if item < 0:
-            continue
-        for i in range(nr):
-            o = int(rows[items[item][3] + row0 + i][0])
-            assert merge_off[o] <= part_slot[part + i] < merge_off[o + 1]
-    row = 0
-    lens = {s: spork.spork_seq_len(c, s) for s in stp.seqs}
-    for s, n in zip(stp.seqs, stp.n_rows):
-        for r in range(n):
-            for h in range(wl.hq):
-                pos = lens[s] - n + r
-                seen = np.zeros(lens[s], dtype=int)
-                for lo, hi in cover[(row + r) * wl.hq + h]:
-                    seen[lo:hi] += 1
-                assert seen[: pos + 1].min() == 1 and seen[: pos + 1].max() == 1
-        row += n
+        r = rows[it[3] + row0: it[3] + row0 + nr]
+        assert r.shape[0] == nr
+        top = np.minimum(hi, r[:, 1] + 1)
+        q_all.append(r[:, 0])
+        lo_all.append(np.full(nr, lo))
+        top_all.append(top)
+        slot_all.append(part_slot[part: part + nr])
+        seqs = row_seq[r[:, 0] // hq]
+        for seq in np.unique(seqs[top > lo]):
+            t = int(top[(seqs == seq) & (top > lo)].max())
+            blk = np.arange(lo // bs, (t - 1) // bs + 1)
+            assert np.all(blk < it[2])
+            assert np.array_equal(tables[it[1] + blk], own[int(seq)][blk]), (seq, lo, t)
+    q, lo, top, slot = (np.concatenate(x) for x in (q_all, lo_all, top_all, slot_all))
+    # merge positions: a permutation, each inside its output's range
+    assert np.array_equal(np.sort(part_slot), np.arange(info["n_partials"]))
+    assert np.all((merge_off[q] <= slot) & (slot < merge_off[q + 1]))
+    assert np.array_equal(np.bincount(q, minlength=n_out), np.diff(merge_off))
+    # coverage: per output the non-empty ranges tile [0, pos] with no gap or overlap
+    keep = top > lo
+    q, lo, top = q[keep], lo[keep], top[keep]
+    order = np.lexsort((lo, q))
+    q, lo, top = q[order], lo[order], top[order]
+    assert np.array_equal(np.unique(q), np.arange(n_out))
+    first = np.r_[True, q[1:] != q[:-1]]
+    last = np.r_[q[1:] != q[:-1], True]
+    assert np.all(lo[first] == 0)
+    assert np.all(lo[~first] == top[np.nonzero(~first)[0] - 1])
+    pos = np.concatenate([np.arange(lens[s] - n, lens[s]) for s, n in zip(stp.seqs, stp.n_rows)])
+    assert np.array_equal(top[last], np.repeat(pos, hq) + 1)
+
+
+def _full_size(case):
+    """A workload at its full size without K/V arrays (the plan needs only
+    the scenario): the five benchmark workloads, the staggered fork tree and
+    its supersession step, the probe prefill and the K = 50 verify."""
+    if case == "tree-supersede":
+        wl = oracle_pool.tight_pool(synth.add_supersession_step(synth.make_tree(kv=False)))
+        assert oracle_pool.reused_blocks(wl)
+        return wl
+    if case == "verify-k50":
+        return synth.make_named("qwen3-32b-verify", verify_k=50, kv=False)
+    if case in ("tree", "prefill"):
+        return synth.make_named(synth.TREE_NAME if case == "tree" else synth.PREFILL_NAME, kv=False)
+    return synth.make(int(case), kv=False)
+
+
+@pytest.mark.parametrize("case", ["0", "1", "2", "3", "4", "tree", "tree-supersede", "prefill", "verify-k50"])
+def test_full_size_plans_cover_every_output(case):
+    """Every step of every full-size workload, planned as the benchmark
+    plans it (256 compute units; the 8-wave re-plan for the many-row steps):
+    coverage, tables and merge ranges as in _check_cover."""
+    wl = _full_size(case)
+    c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
+    shape = spork.make_shape(wl.hq, wl.hkv, wl.d, wl.block_size,
+                             spork.SPORK_DTYPE_BF16 if wl.dtype == synth.BF16 else spork.SPORK_DTYPE_F32,
+                             wl.sm_scale)
+    try:
+        for i, stp in enumerate(wl.steps):
+            for op in stp.ops_before:
+                if op[0] == "new":
+                    spork.spork_seq_new(c)
+                elif op[0] == "append":
+                    spork.spork_seq_append(c, op[1], op[2])
+                elif op[0] == "free":
+                    spork.spork_seq_free(c, op[1])
+                else:
+                    spork.spork_fork(c, op[1])
+            p = spork.spork_plan_create(c, shape, stp.seqs, stp.n_rows, stp.groups, 256)
+            try:
+                info = spork.spork_plan_get_info(p)
+                if case in ("prefill", "verify-k50"):
+                    assert info["attn_waves"] == 8
+                elif wl.dtype == synth.BF16:
+                    assert info["attn_waves"] == 4
+                assert info["unique_kv_bytes"] == wl.unique_kv_bytes(i)
+                _check_cover(wl, c, p, step_index=i)
+            finally:
+                spork.spork_plan_destroy(p)
+    finally:
+        spork.spork_cache_destroy(c)
 
 
 def test_plan_covers_every_output_once_per_token():
@@ -463,6 +523,8 @@ def test_supersession_plan():
     wl = synth.make_tree(sessions=3, prefix=300, stride=40, probes=3, probe_tokens=(1, 20), main_extra=(1, 30),
                          hq=4, hkv=2, d=64, dtype=synth.F32)
     synth.add_supersession_step(wl, seed=2)
+    oracle_pool.tight_pool(wl)
+    assert oracle_pool.reused_blocks(wl)
     c, p = _plan_for(wl, n_cu=8)
     info = spork.spork_plan_get_info(p)
     assert info["unique_kv_bytes"] == wl.unique_kv_bytes(1)

@@ -7,6 +7,7 @@ import pytest
 import torch
 
 from paper_2607_03333_amd import runner, spork, synth
+import oracle_pool
 from gpu_cases import compare_attention, run_workload, say
 
 pytestmark = pytest.mark.gpu
@@ -84,6 +85,7 @@ def test_cascade_matches_flat():
     out = torch.empty_like(dw.steps[0].out)
     lse = torch.empty_like(dw.steps[0].lse)
     ws = torch.empty(info["workspace_bytes"] + 256, dtype=torch.uint8, device=dw.device)
+    spork.spork_workspace_clear(flat_plan, ws)  # control words zero before first use
     spork.spork_attn_decode(flat_plan, img, dw.steps[0].q, dw.k_pool, dw.v_pool, out, lse, ws)
     torch.cuda.synchronize()
     diff = (out.float() - casc).abs().max().item()
@@ -188,10 +190,14 @@ def test_fp32_head_dim_128(block_size):
 def test_supersession_frees_and_reforks(dtype, shape):
     """A second step after a fork tree: the oldest probe of every session is
     freed (its blocks return to the free queue with stale KV), the main thread
-    decodes on and a new probe forks; both steps match the oracle and the
-    block tables and free queue match the oracle manager."""
+    decodes on and a new probe forks; the pool is as small as the scenario
+    allows, so the second step's appends take the freed blocks. Both steps
+    match the oracle and the block tables and free queue match the oracle
+    manager."""
     wl = synth.make_tree(sessions=3, prefix=500, stride=40, probes=3, probe_tokens=(1, 30), main_extra=(1, 40),
                          dtype=dtype, **shape)
     synth.add_supersession_step(wl, seed=1)
-    say(f"supersession {dtype}: step 1 ops {wl.steps[1].ops_before[:4]}")
+    oracle_pool.tight_pool(wl)
+    assert oracle_pool.reused_blocks(wl), "step 1 must reuse freed blocks"
+    say(f"supersession {dtype}: pool {wl.num_blocks} blocks, step 1 reuses {len(oracle_pool.reused_blocks(wl))}")
     run_workload(wl, f"supersede {dtype}").close()
