@@ -175,7 +175,7 @@ typedef struct spork_plan_info {
   int64_t unique_kv_bytes; /* (shared + private tokens) * 2 * Hkv * D * elem */
   int64_t flat_kv_bytes;   /* bytes a kernel without prefix sharing reads */
   int32_t attn_waves;      /* waves per attention workgroup (bf16: 4, two workgroups per
-                              compute unit, or 8 when a range has more than 16 row tiles,
+                              compute unit, or 8 when a range has more than 8 row tiles,
                               one per compute unit; fp32: 1) */
   size_t control_bytes;    /* leading workspace bytes that hold control words (see
                               spork_workspace_clear) */

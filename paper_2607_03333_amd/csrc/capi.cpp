@@ -267,11 +267,11 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
     int rc = check_shape(shape);
     if (rc != SPORK_OK) return rc;
     // bf16: persistent 4-wave workgroups with up to 2 row tiles per wave, two
-    // per compute unit (68 KB of LDS each). When some range has more than 16
-    // row tiles (multi-row probe prefill, verify at K of about 50), the batch
-    // is MFMA-bound and 4-wave workgroups would stream that range in three or
-    // more row slices: it is planned again for one 8-wave workgroup per
-    // compute unit (up to 16 tiles, an 8-stage 128 KB ring). fp32: one 1-wave
+    // per compute unit (68 KB of LDS each). When some range has more than 8
+    // row tiles (verify at K = 16 and more, multi-row probe prefill), 4-wave
+    // workgroups would stream that range once per row slice: the batch is
+    // planned again for one 8-wave workgroup per compute unit (up to 16
+    // tiles in one slice, an 8-stage 128 KB ring). fp32: one 1-wave
     // workgroup per unit with up to 4 row tiles, 4 per CU (8 with up to 2).
     const bool bf16 = shape->dtype == SPORK_DTYPE_BF16;
     auto shape_for = [&](int32_t waves) {
@@ -282,7 +282,7 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
     auto* plan = new spork_plan();
     plan->shape = *shape;
     std::string err = spork::build_plan(cache->bm, shape_for(4), seqs, n_rows, groups, n_threads, n_cu, &plan->p);
-    if (err.empty() && bf16 && plan->p.max_range_tiles > 16) {
+    if (err.empty() && bf16 && plan->p.max_range_tiles > 8) {
       plan->p = spork::Plan{};
       err = spork::build_plan(cache->bm, shape_for(8), seqs, n_rows, groups, n_threads, n_cu, &plan->p);
     }
