@@ -260,6 +260,29 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
                         int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
                         void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* spork_verify_accept without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation). Same arguments and results as
+ * spork_verify_accept (plan may be NULL, n_verify may be 0), same kernels;
+ * the partial results, cursors and argmax keys live in a library-owned
+ * 64 MiB array per GPU (a device global, held until the process ends)
+ * instead of the workspace. A step that needs more (the sum of
+ * info.workspace_bytes rounded up to 256 and spork_verify_workspace_bytes)
+ * is rejected with SPORK_E_CAPACITY before anything is launched; use
+ * spork_verify_accept for it. No device memory is allocated or freed and
+ * no timing events are recorded. The first call on a device looks up that
+ * device's array; a call whose plan needs more zeroed control words than
+ * the previous call left zero launches a small clearing kernel first.
+ * Every call on one GPU shares that GPU's array, which keeps the last
+ * call's contents: calls that overlap on one GPU (different streams or
+ * threads) race and must be serialised by the caller. */
+int spork_verify_accept_noalloc(const spork_plan* plan, const void* dev_image, const void* q,
+                                const void* k_cache, const void* v_cache, void* out, float* lse,
+                                const void* logits, int32_t logits_dtype, int32_t vocab,
+                                const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
+                                int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
+                                hipStream_t stream);
+
 /* Workspace for spork_probe_confidence. */
 int spork_confidence_workspace_bytes(int32_t n_rows, int32_t vocab, size_t* bytes);
 

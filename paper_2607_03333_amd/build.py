@@ -22,7 +22,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["block_manager.cpp", "plan.cpp", "capi.cpp"]
-DEVICE_SOURCES = ["attention.hip", "vocab.hip", "kv.hip", "ngram.hip", "ceiling.hip"]
+DEVICE_SOURCES = ["attention.hip", "vocab.hip", "kv.hip", "ngram.hip", "ceiling.hip", "noalloc.hip"]
 DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                 "-Wno-unused-command-line-argument"]

@@ -14,6 +14,7 @@
 #include "ceiling_kernels.h"
 #include "kernels.h"
 #include "ngram_kernels.h"
+#include "noalloc.h"
 #include "vocab_kernels.h"
 #include "plan.h"
 
@@ -347,9 +348,9 @@ int spork_workspace_clear(const spork_plan* plan, void* workspace, size_t ws_byt
 // Attention over a plan. bf16 (persistent): the attention launch (with the
 // argmax units of a verify step in its tail), then the merge launch (with
 // the accept). fp32: the argmax first (verify), the attention, the merge.
-static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
-                     const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
-                     const spork::AcceptArgs* acc, hipStream_t stream) {
+// Checks of the attention arguments that come before anything is launched.
+static int check_attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                           const void* v_cache, const void* out) {
   const spork::Plan& p = plan->p;
   const spork_shape& sh = plan->shape;
   if (!spork::attention_supported(sh.dtype, sh.head_dim, sh.block_size, p.row_tiles, p.shape.waves))
@@ -359,6 +360,16 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   if ((reinterpret_cast<uintptr_t>(dev_image) & 255) != 0) return fail(SPORK_E_INVAL, "dev_image must be 256-byte aligned");
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
     return fail(SPORK_E_INVAL, "q, pools and out must be 16-byte aligned");
+  return SPORK_OK;
+}
+
+static int attention(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                     const void* v_cache, void* out, float* lse, void* workspace, size_t ws_bytes,
+                     const spork::AcceptArgs* acc, hipStream_t stream) {
+  const spork::Plan& p = plan->p;
+  const spork_shape& sh = plan->shape;
+  int rc0 = check_attention(plan, dev_image, q, k_cache, v_cache, out);
+  if (rc0 != SPORK_OK) return rc0;
   if (ws_bytes < p.workspace_bytes) return fail(SPORK_E_CAPACITY, "workspace smaller than info.workspace_bytes");
   if (p.workspace_bytes > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
     return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
@@ -433,11 +444,16 @@ int spork_verify_workspace_bytes(int32_t n_verify, int32_t k_drafts, int32_t voc
   return SPORK_OK;
 }
 
-int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
-                        const void* v_cache, void* out, float* lse, const void* logits, int32_t logits_dtype,
-                        int32_t vocab, const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
-                        int32_t* accept_len, int32_t* next_token, int32_t* argmax_out, void* workspace,
-                        size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+// The verify step over a caller's workspace, or (scratch = true) over the
+// library's per-device scratch array, in which case `workspace` and
+// `ws_bytes` are ignored.
+static int verify_accept(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                         const void* v_cache, void* out, float* lse, const void* logits, int32_t logits_dtype,
+                         int32_t vocab, const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
+                         int32_t* accept_len, int32_t* next_token, int32_t* argmax_out, void* workspace,
+                         size_t ws_bytes, bool scratch, hipStream_t stream) {
   return guarded([&] {
     if (n_verify < 0 || k_drafts < 0 || k_drafts > 4096 || vocab <= 0)
       return fail(SPORK_E_INVAL, "n_verify >= 0, 0 <= k_drafts <= 4096 and vocab > 0 required");
@@ -451,6 +467,20 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     if (plan != nullptr) att_ws = (plan->p.workspace_bytes + 255) & ~static_cast<size_t>(255);
     size_t acc_ws = 0;
     spork_verify_workspace_bytes(n_verify, k_drafts, vocab, &acc_ws);
+    if (scratch) {
+      if (att_ws + acc_ws > spork::kScratchBytes)
+        return fail(SPORK_E_CAPACITY, "spork_verify_accept_noalloc: the step needs " + std::to_string(att_ws + acc_ws) +
+                                          " bytes of scratch, more than the library's " +
+                                          std::to_string(spork::kScratchBytes) + " (use spork_verify_accept)");
+      if (plan != nullptr) {
+        const int rc = check_attention(plan, dev_image, q, k_cache, v_cache, out);
+        if (rc != SPORK_OK) return rc;
+      }
+      const int rc = hip_status(spork::scratch_acquire(plan != nullptr ? plan->p.control_bytes : 0, stream, &workspace),
+                                "spork_verify_accept_noalloc (scratch)");
+      if (rc != SPORK_OK) return rc;
+      ws_bytes = spork::kScratchBytes;
+    }
     if (ws_bytes < att_ws + acc_ws) return fail(SPORK_E_CAPACITY, "workspace too small for attention + accept");
     if ((att_ws + acc_ws) > 0 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
       return fail(SPORK_E_INVAL, "workspace must be non-NULL and 256-byte aligned");
@@ -475,6 +505,31 @@ int spork_verify_accept(const spork_plan* plan, const void* dev_image, const voi
     return hip_status(timed(SPORK_KERNEL_ACCEPT, stream, [&] { return spork::launch_accept_tail(a, stream); }),
                       "spork_verify_accept (accept)");
   });
+}
+
+extern "C" {
+
+int spork_verify_accept(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                        const void* v_cache, void* out, float* lse, const void* logits, int32_t logits_dtype,
+                        int32_t vocab, const int32_t* drafts, int32_t n_verify, int32_t k_drafts,
+                        int32_t* accept_len, int32_t* next_token, int32_t* argmax_out, void* workspace,
+                        size_t ws_bytes, hipStream_t stream) {
+  return verify_accept(plan, dev_image, q, k_cache, v_cache, out, lse, logits, logits_dtype, vocab, drafts, n_verify,
+                       k_drafts, accept_len, next_token, argmax_out, workspace, ws_bytes, false, stream);
+}
+
+int spork_verify_accept_noalloc(const spork_plan* plan, const void* dev_image, const void* q, const void* k_cache,
+                                const void* v_cache, void* out, float* lse, const void* logits,
+                                int32_t logits_dtype, int32_t vocab, const int32_t* drafts, int32_t n_verify,
+                                int32_t k_drafts, int32_t* accept_len, int32_t* next_token, int32_t* argmax_out,
+                                hipStream_t stream) {
+  // No timing events here: creating one may allocate.
+  const bool timing = g_timing.on;
+  g_timing.on = false;
+  const int rc = verify_accept(plan, dev_image, q, k_cache, v_cache, out, lse, logits, logits_dtype, vocab, drafts,
+                               n_verify, k_drafts, accept_len, next_token, argmax_out, nullptr, 0, true, stream);
+  g_timing.on = timing;
+  return rc;
 }
 
 int spork_confidence_workspace_bytes(int32_t n_rows, int32_t vocab, size_t* bytes) {

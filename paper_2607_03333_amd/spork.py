@@ -93,6 +93,8 @@ _SIGNATURES = {
                                                     ctypes.POINTER(ctypes.c_size_t)]),
     "spork_verify_accept": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _c_i32, _c_i32, _p,
                                            _c_i32, _c_i32, _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "spork_verify_accept_noalloc": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _c_i32, _c_i32, _p,
+                                                   _c_i32, _c_i32, _p, _p, _p, _p]),
     "spork_confidence_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i32,
                                                         ctypes.POINTER(ctypes.c_size_t)]),
     "spork_probe_confidence": (ctypes.c_int, [_p, _c_i32, _c_i32, _c_i32, _p, _c_i32, ctypes.c_float,
@@ -300,6 +302,14 @@ def spork_verify_accept(plan, dev_image, q, k_cache, v_cache, out, lse, logits, 
                                      _ptr(drafts), n_verify, k_drafts, _ptr(accept_len),
                                      _ptr(next_token), _ptr(argmax_out), _ptr(workspace), ws_bytes,
                                      _stream(stream)))
+
+
+def spork_verify_accept_noalloc(plan, dev_image, q, k_cache, v_cache, out, lse, logits, logits_dtype, vocab,
+                                drafts, n_verify, k_drafts, accept_len, next_token, argmax_out, stream=None):
+    _check(lib().spork_verify_accept_noalloc(plan, _ptr(dev_image), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                             _ptr(out), _ptr(lse), _ptr(logits), logits_dtype, vocab,
+                                             _ptr(drafts), n_verify, k_drafts, _ptr(accept_len),
+                                             _ptr(next_token), _ptr(argmax_out), _stream(stream)))
 
 
 def spork_confidence_workspace_bytes(n_rows, vocab):

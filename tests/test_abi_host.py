@@ -210,6 +210,34 @@ def test_read_ceiling_error_codes():
     assert e.value.code == spork.SPORK_E_INVAL
 
 
+def test_noalloc_rejects_steps_beyond_its_scratch():
+    """The no-allocation verify entry point refuses a step whose partial
+    results would not fit its 64 MiB per-device scratch (the full-size probe
+    prefill needs about 272 MiB) before touching the GPU, and checks its
+    pointers like spork_verify_accept."""
+    wl = synth.make_prefill(kv=False)
+    stp = wl.steps[0]
+    c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
+    for op in stp.ops_before:
+        {"new": lambda o: spork.spork_seq_new(c), "append": lambda o: spork.spork_seq_append(c, o[1], o[2]),
+         "fork": lambda o: spork.spork_fork(c, o[1])}[op[0]](op)
+    shape = spork.make_shape(wl.hq, wl.hkv, wl.d, wl.block_size, spork.SPORK_DTYPE_BF16, wl.sm_scale)
+    p = spork.spork_plan_create(c, shape, stp.seqs, stp.n_rows, stp.groups, 256)
+    try:
+        assert spork.spork_plan_get_info(p)["workspace_bytes"] > (64 << 20)
+        with pytest.raises(spork.SporkError) as e:
+            spork.spork_verify_accept_noalloc(p, 256, 256, 256, 256, 256, 256, 256, spork.SPORK_DTYPE_BF16, 1000,
+                                              256, 0, 0, 256, 256, None, stream=0)
+        assert e.value.code == spork.SPORK_E_CAPACITY and "scratch" in str(e.value)
+        with pytest.raises(spork.SporkError) as e:   # NULL logits with verify threads
+            spork.spork_verify_accept_noalloc(None, None, None, None, None, None, None, None, spork.SPORK_DTYPE_BF16,
+                                              1000, 256, 4, 2, 256, 256, None, stream=0)
+        assert e.value.code == spork.SPORK_E_INVAL
+    finally:
+        spork.spork_plan_destroy(p)
+        spork.spork_cache_destroy(c)
+
+
 def _plan_for(wl, groups=None, n_cu=256):
     c = spork.spork_cache_create(wl.num_blocks, wl.block_size, wl.free_order)
     for stp in wl.steps:
