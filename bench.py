@@ -260,6 +260,100 @@ def ngram_bench(args, torch, spork, synth):
                      "avg_launch_ms": round(ms_scan, 4), "algorithmic_bytes_per_launch": nbytes}}), flush=True)
 
 
+def decode_bench(args, torch, spork, synth, runner):
+    """A decode loop on one plan: after the workload's step, ``--decode-steps``
+    more steps in which every thread appends one token (the host block
+    manager), its K/V is written (kv write kernel), the plan is advanced
+    (spork_plan_advance: host checks plus one small patch kernel) and the
+    step runs. Reports the host time of the appends and the advance against
+    the GPU time of the patch and the step, and checks sampled threads of the
+    last step against the oracle. The steps are enqueued back to back; the
+    host work of step i overlaps the GPU work of earlier steps."""
+    import numpy as np
+
+    import oracle
+    n = args.decode_steps
+    wl = synth.make_named(args.workload, **({"verify_k": args.verify_k} if args.verify_k else {}))
+    synth.add_decode_steps(wl, n)
+    dw = runner.DeviceWorkload(wl, poison_pool=False)
+    step = dw.prepare(0)
+    units = step.info["n_units"]
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    seqs = list(wl.steps[0].seqs)
+    ones = [1] * len(seqs)
+    # The new tokens' K/V and Q reach the device before the loop (a model's
+    # forward pass writes them there); pinned buffers carry each step's slots.
+    k_new, v_new, q_new, pinned = [], [], [], []
+    for i in range(1, n + 1):
+        k_new.append(runner.to_device(np.stack([wl.suffix_k[q][len(wl.suffix_k[q]) - n + i - 1] for q in seqs]),
+                                      wl.dtype, dw.device))
+        v_new.append(runner.to_device(np.stack([wl.suffix_v[q][len(wl.suffix_v[q]) - n + i - 1] for q in seqs]),
+                                      wl.dtype, dw.device))
+        q_new.append(runner.to_device(wl.steps[i].q, wl.dtype, dw.device))
+        pinned.append(torch.empty(len(seqs), dtype=torch.int64, pin_memory=True))
+    torch.cuda.synchronize()
+    host_append, host_advance, ev = [], [], []
+    for i in range(1, n + 1):
+        t0 = time.perf_counter()
+        slots, cows = spork.spork_seq_append_batch(dw.cache, seqs, ones)
+        t1 = time.perf_counter()
+        assert not cows, "a decode append copied a shared block"
+        pinned[i - 1].numpy()[:] = slots
+        slots_d = pinned[i - 1].to(dw.device, non_blocking=True)
+        spork.spork_kv_write(dw.shape, dw.k_pool, dw.v_pool, wl.num_blocks, slots_d, k_new[i - 1], v_new[i - 1],
+                             dw.bad_slots)
+        step.q.copy_(q_new[i - 1])
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        t2 = time.perf_counter()
+        spork.spork_plan_advance(step.plan, dw.cache, step.image)
+        t3 = time.perf_counter()
+        step.index, step.spec = i, wl.steps[i]
+        step.run()
+        b.record(stream)
+        host_append.append((t1 - t0) * 1e3)
+        host_advance.append((t3 - t2) * 1e3)
+        ev.append((a, b))
+    torch.cuda.synchronize()
+    gpu = [a.elapsed_time(b) for a, b in ev]
+    info = spork.spork_plan_get_info(step.plan)
+    assert info["n_units"] == units and int(dw.bad_slots.item()) == 0
+    # oracle parity on sampled threads of the last step
+    stl = wl.steps[n]
+    starts = np.concatenate([[0], np.cumsum(stl.n_rows)])
+    out = step.out.float().cpu().numpy().astype(np.float64)
+    worst = 0.0
+    pick = sorted({0, len(stl.seqs) // 2, len(stl.seqs) - 1})
+    for t in pick:
+        seq, r0, nr = stl.seqs[t], int(starts[t]), stl.n_rows[t]
+        k, v = wl.context(seq, wl.thread_len(seq, n))
+        o, _ = oracle.attend(synth.to_f64(stl.q[r0:r0 + nr], wl.dtype), synth.to_f64(k, wl.dtype),
+                             synth.to_f64(v, wl.dtype), wl.sm_scale)
+        worst = max(worst, float(np.abs(out[r0:r0 + nr] - o).max()))
+    tol = 1e-5 if wl.dtype == synth.F32 else 2e-2
+    med = float(np.median(gpu))
+    host = float(np.median(np.array(host_append) + np.array(host_advance)))
+    print(json.dumps({
+        "metric": "decode loop on one plan: host ms per step vs GPU ms per step", "value": round(host / med, 4),
+        "unit": "host/GPU time ratio", "n_gpus": 1, "steps": n, "warmup": args.warmup, "ms_per_step": round(med, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == synth.BF16 else "f32", "data": "synthetic (seeded Gaussian K/V/Q)",
+        "config": {"workload": wl.name, "decode_steps": n, "threads": len(stl.seqs), "units": units},
+        "gpu_ms_per_step": {"median": round(med, 4), "min": round(float(np.min(gpu)), 4),
+                            "what": "plan patch kernel + attention step (events)"},
+        "host_ms_per_step": {"append_batch_median": round(float(np.median(host_append)), 4),
+                             "advance_median": round(float(np.median(host_advance)), 4),
+                             "total_median": round(host, 4)},
+        "unique_kv_bytes_last_step": info["unique_kv_bytes"],
+        "last_step_parity": {"threads": pick, "max_abs": worst, "tol": tol, "ok": worst <= tol}}), flush=True)
+    dw.close()
+    if worst > tol:
+        sys.exit(1)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,6 +370,9 @@ def main():
     ap.add_argument("--confidence-probes", type=int, default=0,
                     help="instead of the benchmark, time the D2 confidence gate over this many probe "
                          "spans (0..16 positions each) of the 151,936-token vocabulary, bf16 logits")
+    ap.add_argument("--decode-steps", type=int, default=0,
+                    help="instead of the benchmark, run this many decode steps on one plan after the "
+                         "workload's step (spork_plan_advance) and time host against GPU work")
     ap.add_argument("--ngram-seqs", type=int, default=0,
                     help="instead of the benchmark, time the n-gram draft proposer over this many "
                          "token histories of 32768-36864 tokens")
@@ -311,6 +408,9 @@ def main():
         return
     if args.ngram_seqs:
         ngram_bench(args, torch, spork, synth)
+        return
+    if args.decode_steps:
+        decode_bench(args, torch, spork, synth, runner)
         return
 
     t_gen = time.perf_counter()

@@ -109,6 +109,18 @@ int spork_seq_new(spork_cache* cache, int32_t* seq_out);
 int spork_seq_append(spork_cache* cache, int32_t seq, int32_t n_tokens, int64_t* slots_out,
                      int32_t* cow_out, int32_t* n_cow_out);
 
+/* Appends to n_seqs distinct sequences (host arrays seqs, n_tokens), in
+ * order, with the same result as one spork_seq_append per sequence, for a
+ * decode step's bookkeeping in one call. slots_out (host int64, sum of
+ * n_tokens entries) receives the slots in batch order; cow_out (host int32,
+ * 3 * n_seqs entries) receives *n_cow_out (src, dst, n_valid) copies, in
+ * batch order, for spork_kv_copy. All or nothing: the blocks the batch needs
+ * are counted first (a copy made unnecessary by an earlier append of the
+ * batch is not counted), SPORK_E_NOBLOCKS leaves the cache unchanged;
+ * SPORK_E_INVAL for an unknown or repeated sequence or a negative count. */
+int spork_seq_append_batch(spork_cache* cache, const int32_t* seqs, const int32_t* n_tokens,
+                           int32_t n_seqs, int64_t* slots_out, int32_t* cow_out, int32_t* n_cow_out);
+
 /* Copy-on-write fork (Section 4.1, D1): a new sequence whose table is a copy
  * of parent's; every referenced block gains one reference; no KV is copied. */
 int spork_fork(spork_cache* cache, int32_t parent_seq, int32_t* child_seq_out);
@@ -192,6 +204,28 @@ int spork_plan_create(const spork_cache* cache, const spork_shape* shape, const 
                       int32_t n_cu, spork_plan** out);
 int spork_plan_destroy(spork_plan* plan);
 int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info);
+
+/* Reuse a plan for a later decode step (Sections 4.1 and 4.3: every main
+ * and probe thread keeps decoding; the batch stays the same).
+ * After tokens were appended to the plan's threads (spork_seq_append on
+ * `cache`, the cache the plan was made from), bring the plan and its device
+ * image up to the threads' current lengths: each thread's private range
+ * (the part of its context no other thread of its group shares), its rows'
+ * positions (still the last n_rows[t] positions of the context) and its
+ * block table grow with it. The work split is kept, so this costs
+ * O(threads + new blocks) host time and, when anything changed, one small
+ * kernel on `stream` per 480 changed words of `dev_image` (the device copy
+ * of spork_plan_image, 256-byte aligned; the patch travels in the kernel's
+ * arguments, nothing is copied from the host). Call it after the appends
+ * and before the step's attention call, on the same stream.
+ * SPORK_E_CAPACITY when the plan cannot absorb the growth: more new blocks
+ * than the 64 the image reserves per thread table, a private range past
+ * the longest unit the kernel stages, or a grown thread with no private
+ * range; SPORK_E_INVAL when a planned sequence was freed, shrank or had a
+ * planned block replaced (copy-on-write). In both cases nothing is launched,
+ * the plan is unchanged, and the caller plans again. */
+int spork_plan_advance(spork_plan* plan, const spork_cache* cache, void* dev_image,
+                       hipStream_t stream);
 
 /* Copy the plan's device image (block tables, work list, merge lists) into
  * host_dst (cap bytes, >= info.image_bytes). The caller places it in device

@@ -91,7 +91,7 @@ __device__ __forceinline__ void wait_stage(int after);
 // MI355X against 5.9 TB/s with the default policy (measured with the
 // direct-to-LDS read-ceiling kernel in the same ring shape).
 constexpr int kNonTemporal = 2;
-constexpr int kUnitBlocks = 1040;   // block-table entries a unit may span (see kMaxUnitTokens)
+constexpr int kUnitBlocks = kUnitTableEntries;   // block-table entries a unit may span (see kMaxUnitTokens)
 constexpr float kRescaleSlack = 8.0f;  // base-2 headroom before the reference max moves
 constexpr float kRescaleSum = 256.0f;  // 2^kRescaleSlack: bound on a lane's 8 probabilities of a row
 
@@ -221,7 +221,11 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   const uint16_t* __restrict__ kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* __restrict__ vc = static_cast<const uint16_t*>(a.v_cache);
   const int32_t* __restrict__ table = a.tables + it.table_off;
-  const int nb = it.n_blocks;
+  // Tokens appended to a private range's thread since the plan was made: the
+  // range's last unit, its rows' horizons and its table grow by them.
+  const int grow = it.grow;
+  const int tok_hi = w.tok_hi == it.hi ? w.tok_hi + grow : w.tok_hi;
+  const int nb = grow != 0 ? (it.hi + grow + BS - 1) / BS : it.n_blocks;
   const size_t head = static_cast<size_t>(it.kv_head);
   const size_t hkv = static_cast<size_t>(a.hkv);
   const int ntiles = (w.nrows + 15) >> 4;
@@ -239,7 +243,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     slot[j] = 0;
     if (own[j] && i < w.nrows) {
       const RowDesc rd = a.rows[it.row_off + w.row0 + i];
-      hz[j] = rd.horizon;
+      hz[j] = rd.horizon + grow;
       slot[j] = a.part_slot[w.partial + i];
       const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rd.qidx) * D);
 #pragma unroll
@@ -269,7 +273,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   }
 
   const int tb0 = w.tok_lo & ~(kTileTokens - 1);
-  const int nstage = (w.tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
+  const int nstage = (tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
 
   // This lane's 4 chunks of a stage: instruction k of wave w fills chunks
   // (4w + k)*64 + lane. Waves 0-1: K chunks (token t, channel group c);
@@ -351,7 +355,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     constexpr int NT = decltype(nt_c)::value;
     const int tb = tb0 + st * kTileTokens;
     const uint32_t soff = static_cast<uint32_t>(st % kRing) * (kStageChunks * 16);
-    const bool edge = tb < w.tok_lo || tb + kTileTokens > w.tok_hi || tb + kTileTokens - 1 > hmin;
+    const bool edge = tb < w.tok_lo || tb + kTileTokens > tok_hi || tb + kTileTokens - 1 > hmin;
     u32x4 kr[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) kr[i] = lds_read_b128(kaddr[i] + soff);
@@ -388,7 +392,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int tk = tb + 8 * g + e;
-        if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[j]) sv[j][e] = kNegInf;
+        if (tk < w.tok_lo || tk >= tok_hi || tk > hz[j]) sv[j][e] = kNegInf;
       }
     };
     // Softmax of tile j: the lane's 8 probabilities of its row against the
@@ -454,10 +458,10 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     // Positions past the range may hold anything: zero their V (0 * NaN
     // would poison the accumulator).
     auto zero_past_range = [&]() __attribute__((always_inline)) {
-      if (tb + kTileTokens > w.tok_hi) {
+      if (tb + kTileTokens > tok_hi) {
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          const uint4 z = zero_past(make_uint4(vr[dt][0], vr[dt][1], vr[dt][2], vr[dt][3]), tb + 8 * g, w.tok_hi);
+          const uint4 z = zero_past(make_uint4(vr[dt][0], vr[dt][1], vr[dt][2], vr[dt][3]), tb + 8 * g, tok_hi);
           vr[dt] = u32x4{z.x, z.y, z.z, z.w};
         }
       }
@@ -597,7 +601,9 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
   const float* __restrict__ kc = static_cast<const float*>(a.k_cache);
   const float* __restrict__ vc = static_cast<const float*>(a.v_cache);
   const int32_t* __restrict__ table = a.tables + it.table_off;
-  const int nb = it.n_blocks;
+  const int grow = it.grow;  // tokens appended since the plan (see the bf16 kernel)
+  const int tok_hi = w.tok_hi == it.hi ? w.tok_hi + grow : w.tok_hi;
+  const int nb = grow != 0 ? (it.hi + grow + BS - 1) / BS : it.n_blocks;
   const size_t head = static_cast<size_t>(it.kv_head);
   const size_t hkv = static_cast<size_t>(a.hkv);
   const int ntiles = (w.nrows + 15) >> 4;
@@ -609,7 +615,7 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
     const int i = t * 16 + r16;
     if (i < w.nrows) {
       const RowDesc rd = a.rows[it.row_off + w.row0 + i];
-      hz[t] = rd.horizon;
+      hz[t] = rd.horizon + grow;
       const float* qp = qg + static_cast<size_t>(rd.qidx) * D;
 #pragma unroll
       for (int s = 0; s < KS; ++s) qop[t][s] = qp[4 * s + g];
@@ -641,7 +647,7 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
   };
 
   const float c = a.scale_log2;
-  for (int tb = w.tok_lo & ~(kTileTokens - 1); tb < w.tok_hi; tb += kTileTokens) {
+  for (int tb = w.tok_lo & ~(kTileTokens - 1); tb < tok_hi; tb += kTileTokens) {
     const size_t b0 = blk(tb, 0);
     const size_t b1 = BS == 16 ? blk(tb, 1) : b0;
     float kop[2][KS];
@@ -658,15 +664,15 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         f32x4 v = *reinterpret_cast<const f32x4*>(vp + static_cast<size_t>(16 * dt + r16) * BS);
-        if (tb + kTileTokens > w.tok_hi) {
+        if (tb + kTileTokens > tok_hi) {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            if (tb + 16 * hh + 4 * g + i >= w.tok_hi) v[i] = 0.0f;
+            if (tb + 16 * hh + 4 * g + i >= tok_hi) v[i] = 0.0f;
         }
         vop[hh][dt] = v;
       }
     }
-    const bool edge = tb < w.tok_lo || tb + kTileTokens > w.tok_hi || tb + kTileTokens - 1 > hmin;
+    const bool edge = tb < w.tok_lo || tb + kTileTokens > tok_hi || tb + kTileTokens - 1 > hmin;
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
       if (t < ntiles) {
@@ -687,7 +693,7 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int tk = tb + 16 * hh + 4 * g + i;
-              if (tk < w.tok_lo || tk >= w.tok_hi || tk > hz[t]) sv[4 * hh + i] = kNegInf;
+              if (tk < w.tok_lo || tk >= tok_hi || tk > hz[t]) sv[4 * hh + i] = kNegInf;
             }
         }
         const float alpha = softmax_step(sv, m[t], l[t]);

@@ -1,5 +1,8 @@
 #include "block_manager.h"
 
+#include <unordered_map>
+#include <unordered_set>
+
 namespace spork {
 
 BlockManager::BlockManager(int32_t num_blocks, int32_t block_size, const int32_t* free_order)
@@ -51,6 +54,42 @@ BmStatus BlockManager::append(int32_t seq, int32_t n, int64_t* slots, CowCopy* c
     slots[i] = static_cast<int64_t>(s.table[pos / bs]) * bs + pos % bs;
   }
   s.length += n;
+  return BmStatus::kOk;
+}
+
+BmStatus BlockManager::append_batch(const int32_t* seqs, const int32_t* n, int32_t k, int64_t* slots, CowCopy* cows,
+                                    int32_t* n_cows) {
+  *n_cows = 0;
+  if (k < 0) return BmStatus::kBadArg;
+  const int32_t bs = block_size_;
+  std::unordered_set<int32_t> seen;
+  std::unordered_map<int32_t, int32_t> dref;  // tail blocks released by earlier copies of this batch
+  int64_t need = 0;
+  for (int32_t i = 0; i < k; ++i) {
+    auto it = seqs_.find(seqs[i]);
+    if (it == seqs_.end()) return BmStatus::kUnknownSeq;
+    if (n[i] < 0 || !seen.insert(seqs[i]).second) return BmStatus::kBadArg;
+    if (n[i] == 0) continue;
+    const Seq& s = it->second;
+    if (s.length % bs != 0) {
+      const int32_t tail = s.table.back();
+      if (ref_[tail] + dref[tail] > 1) {
+        need += 1;
+        dref[tail] -= 1;
+      }
+    }
+    need += (static_cast<int64_t>(s.length) + n[i] + bs - 1) / bs - (static_cast<int64_t>(s.length) + bs - 1) / bs;
+  }
+  if (need > static_cast<int64_t>(free_.size())) return BmStatus::kNoBlocks;
+  int64_t at = 0;
+  for (int32_t i = 0; i < k; ++i) {
+    CowCopy cow;
+    int32_t nc = 0;
+    const BmStatus st = append(seqs[i], n[i], slots + at, &cow, &nc);
+    if (st != BmStatus::kOk) return st;  // not reached: the batch was counted above
+    if (nc) cows[(*n_cows)++] = cow;
+    at += n[i];
+  }
   return BmStatus::kOk;
 }
 

@@ -13,6 +13,7 @@
 #include <deque>
 #include <string>
 #include <unordered_map>
+#include <unordered_set>
 #include <vector>
 
 namespace spork {
@@ -32,6 +33,12 @@ class BlockManager {
 
   int32_t seq_new();
   BmStatus append(int32_t seq, int32_t n, int64_t* slots, CowCopy* cow, int32_t* n_cow);
+  // Appends to several distinct sequences, in order, exactly as the single
+  // appends would run; all or nothing (the blocks needed are counted first,
+  // copies that an earlier append of the batch makes unnecessary included).
+  // slots: sum of n[i] entries in batch order; cows: up to k entries, *n_cows set.
+  BmStatus append_batch(const int32_t* seqs, const int32_t* n, int32_t k, int64_t* slots, CowCopy* cows,
+                        int32_t* n_cows);
   BmStatus fork(int32_t parent, int32_t* child);
   BmStatus free_seq(int32_t seq);
 

@@ -2,6 +2,7 @@
 // reporting, block-manager and planner calls, kernel dispatch.
 #include "spork.h"
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstring>
@@ -171,6 +172,30 @@ int spork_seq_append(spork_cache* cache, int32_t seq, int32_t n_tokens, int64_t*
   });
 }
 
+int spork_seq_append_batch(spork_cache* cache, const int32_t* seqs, const int32_t* n_tokens, int32_t n_seqs,
+                           int64_t* slots_out, int32_t* cow_out, int32_t* n_cow_out) {
+  return guarded([&] {
+    if (cache == nullptr || n_cow_out == nullptr || n_seqs < 0) return fail(SPORK_E_INVAL, "NULL argument or n_seqs < 0");
+    if (n_seqs > 0 && (seqs == nullptr || n_tokens == nullptr || cow_out == nullptr))
+      return fail(SPORK_E_INVAL, "NULL argument");
+    int64_t total = 0;
+    for (int32_t i = 0; i < n_seqs; ++i) total += n_tokens[i] > 0 ? n_tokens[i] : 0;
+    if (total > 0 && slots_out == nullptr) return fail(SPORK_E_INVAL, "slots_out is NULL");
+    std::vector<spork::CowCopy> cows(static_cast<size_t>(n_seqs));
+    int32_t n_cow = 0;
+    const int rc = from_bm(cache->bm.append_batch(seqs, n_tokens, n_seqs, slots_out, cows.data(), &n_cow),
+                           "spork_seq_append_batch");
+    if (rc != SPORK_OK) return rc;
+    for (int32_t i = 0; i < n_cow; ++i) {
+      cow_out[3 * i] = cows[i].src;
+      cow_out[3 * i + 1] = cows[i].dst;
+      cow_out[3 * i + 2] = cows[i].n_valid;
+    }
+    *n_cow_out = n_cow;
+    return SPORK_OK;
+  });
+}
+
 int spork_fork(spork_cache* cache, int32_t parent_seq, int32_t* child_seq_out) {
   return guarded([&] {
     if (cache == nullptr || child_seq_out == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
@@ -323,6 +348,86 @@ int spork_plan_get_info(const spork_plan* plan, spork_plan_info* info) {
   info->flat_kv_bytes = p.flat_tokens * per_tok;
   info->control_bytes = p.control_bytes;
   return SPORK_OK;
+}
+
+int spork_plan_advance(spork_plan* plan, const spork_cache* cache, void* dev_image, hipStream_t stream) {
+  return guarded([&] {
+    if (plan == nullptr || cache == nullptr) return fail(SPORK_E_INVAL, "NULL argument");
+    spork::Plan& p = plan->p;
+    const spork::BlockManager& bm = cache->bm;
+    if (dev_image == nullptr || (reinterpret_cast<uintptr_t>(dev_image) & 255) != 0)
+      return fail(SPORK_E_INVAL, "dev_image must be non-NULL and 256-byte aligned");
+    if (bm.block_size() != p.shape.block_size) return fail(SPORK_E_INVAL, "cache block size differs from the plan's");
+    const size_t n = p.seqs.size();
+    std::vector<int32_t> g(n, 0);
+    // Every check first: on an error nothing is launched and the plan is unchanged.
+    for (size_t t = 0; t < n; ++t) {
+      const int32_t seq = p.seqs[t];
+      if (!bm.has(seq)) return fail(SPORK_E_INVAL, "spork_plan_advance: a planned sequence was freed; plan again");
+      g[t] = bm.length(seq) - p.len[t];
+      if (g[t] < 0) return fail(SPORK_E_INVAL, "spork_plan_advance: a sequence is shorter than planned; plan again");
+      if (g[t] > 0 && p.thread_items[t].empty())
+        return fail(SPORK_E_CAPACITY, "spork_plan_advance: a grown thread has no private range to extend; plan again");
+      if (p.thread_table_off[t] >= 0) {
+        // The block manager changes a live table only by appending entries
+        // and by copying the block an append writes into, the last one: the
+        // planned entries are unchanged when the last of them is.
+        const auto& cur = bm.table(seq);
+        const auto& have = p.thread_table[t];
+        if (cur.size() < have.size() || (!have.empty() && cur[have.size() - 1] != have.back()))
+          return fail(SPORK_E_INVAL, "spork_plan_advance: planned blocks changed (copy-on-write or free); plan again");
+        if (static_cast<int64_t>(cur.size()) > p.thread_table_cap[t])
+          return fail(SPORK_E_CAPACITY, "spork_plan_advance: more new blocks than the plan reserves; plan again");
+      }
+    }
+    const auto* waves = reinterpret_cast<const spork::WaveDesc*>(p.image.data() + p.off_waves);
+    auto* items = reinterpret_cast<spork::ItemDesc*>(p.image.data() + p.off_items);
+    for (int32_t u : p.open_units) {
+      const spork::WaveDesc& w = waves[u];
+      const int32_t t = items[w.item].thread;
+      if (spork::unit_table_span(w.tok_lo, w.tok_hi + g[t], p.shape.block_size) > spork::kUnitTableEntries)
+        return fail(SPORK_E_CAPACITY, "spork_plan_advance: a private range outgrew its unit; plan again");
+    }
+    // Patches: each grown thread's `grow` in its private items, the new
+    // entries of its table; written into the host image too.
+    std::vector<std::pair<int32_t, int32_t>> patch;
+    auto* words = reinterpret_cast<int32_t*>(p.image.data());
+    const int32_t items_w = static_cast<int32_t>(p.off_items / 4), tables_w = static_cast<int32_t>(p.off_tables / 4);
+    int64_t added = 0;
+    for (size_t t = 0; t < n; ++t) {
+      if (g[t] != p.grow[t]) {
+        for (int32_t i : p.thread_items[t]) patch.push_back({items_w + i * 8 + 6, g[t]});
+        added += g[t] - p.grow[t];
+      }
+      if (p.thread_table_off[t] >= 0) {
+        const auto& cur = bm.table(p.seqs[t]);
+        for (size_t k = p.thread_table[t].size(); k < cur.size(); ++k)
+          patch.push_back({tables_w + p.thread_table_off[t] + static_cast<int32_t>(k), cur[k]});
+      }
+    }
+    for (size_t i = 0; i < patch.size(); i += spork::kPatchMax) {
+      spork::ImagePatch ip{};
+      ip.n = static_cast<int32_t>(std::min<size_t>(spork::kPatchMax, patch.size() - i));
+      for (int32_t k = 0; k < ip.n; ++k) {
+        ip.off[k] = patch[i + k].first;
+        ip.val[k] = patch[i + k].second;
+      }
+      const int rc = hip_status(spork::launch_image_patch(static_cast<int32_t*>(dev_image), ip, stream),
+                                "spork_plan_advance");
+      if (rc != SPORK_OK) return rc;  // earlier patches of this call may have run; plan again
+    }
+    for (const auto& pw : patch) words[pw.first] = pw.second;
+    for (size_t t = 0; t < n; ++t) {
+      p.grow[t] = g[t];
+      if (p.thread_table_off[t] >= 0) {
+        const auto& cur = bm.table(p.seqs[t]);
+        p.thread_table[t].insert(p.thread_table[t].end(), cur.begin() + p.thread_table[t].size(), cur.end());
+      }
+    }
+    p.private_tokens += added;
+    p.flat_tokens += added;
+    return SPORK_OK;
+  });
 }
 
 int spork_plan_image(const spork_plan* plan, void* host_dst, size_t cap) {

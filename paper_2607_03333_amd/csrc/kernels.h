@@ -72,6 +72,16 @@ int32_t accept_chunks(int32_t rows, int32_t vocab);
 hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream);
 hipError_t launch_accept_tail(const AcceptArgs& a, hipStream_t stream);
 
+// Up to kPatchMax word writes (word offset, value) into a plan's device
+// image, carried in the kernel argument (under 4 KB).
+constexpr int kPatchMax = 480;
+struct ImagePatch {
+  int32_t n;
+  int32_t off[kPatchMax];
+  int32_t val[kPatchMax];
+};
+hipError_t launch_image_patch(int32_t* image, const ImagePatch& patch, hipStream_t stream);
+
 hipError_t launch_kv_write(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
                            int64_t num_slots, void* k_cache, void* v_cache, const int64_t* slots,
                            const void* k_new, const void* v_new, int32_t n, int32_t* bad_slots,

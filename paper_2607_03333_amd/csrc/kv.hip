@@ -50,7 +50,19 @@ __global__ void __launch_bounds__(256) kv_copy_kernel(int hkv, int D, int BS, T*
   vc[vd] = vc[vs];
 }
 
+// Word writes into a plan's device image (spork_plan_advance): the patch
+// travels as the kernel's argument, so nothing is copied from the host.
+__global__ void __launch_bounds__(256) image_patch_kernel(int32_t* image, ImagePatch patch) {
+  for (int i = threadIdx.x; i < patch.n; i += 256) image[patch.off[i]] = patch.val[i];
+}
+
 }  // namespace
+
+hipError_t launch_image_patch(int32_t* image, const ImagePatch& patch, hipStream_t stream) {
+  if (patch.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(image_patch_kernel, dim3(1), dim3(256), 0, stream, image, patch);
+  return hipGetLastError();
+}
 
 hipError_t launch_kv_write(int32_t dtype, int32_t hkv, int32_t head_dim, int32_t block_size,
                            int64_t num_slots, void* k_cache, void* v_cache, const int64_t* slots,

@@ -35,6 +35,12 @@ int32_t cut_piece(int32_t lo, int32_t rest_hi, int64_t want, int64_t min_piece) 
 
 }  // namespace
 
+int32_t unit_table_span(int32_t tok_lo, int32_t tok_hi, int32_t block_size) {
+  const int32_t tb0 = tok_lo / kTileTokens * kTileTokens;
+  const int32_t span_end = tb0 + (tok_hi - tb0 + kTileTokens - 1) / kTileTokens * kTileTokens + 16;
+  return span_end / block_size - tb0 / block_size + 1;
+}
+
 std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int32_t* seqs,
                        const int32_t* n_rows, const int32_t* groups, int32_t n_threads,
                        int32_t n_cu, Plan* out) {
@@ -159,12 +165,20 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   const int32_t slice_rows = row_tiles * 16;
   p.row_tiles = row_tiles;
 
-  // Items (range x KV head), their rows and the block tables.
+  // Items (range x KV head), their rows and the block tables. Each copied
+  // table keeps kTableReserve free entries behind it for the blocks later
+  // decode steps append (spork_plan_advance).
   std::vector<int32_t> table_off(n_threads, -1);
   std::vector<int32_t> tables;
   std::vector<ItemDesc> items;
   std::vector<RowDesc> rows;
   std::vector<Range*> item_range;
+  p.seqs.assign(seqs, seqs + n_threads);
+  p.len = len;
+  p.thread_items.assign(n_threads, {});
+  p.thread_table.assign(n_threads, {});
+  p.thread_table_off.assign(n_threads, -1);
+  p.thread_table_cap.assign(n_threads, 0);
   for (size_t r = 0; r < ranges.size(); ++r) {
     Range& rg = ranges[r];
     const int32_t tt = rg.table_thread;
@@ -172,7 +186,12 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
       table_off[tt] = static_cast<int32_t>(tables.size());
       const auto& tb = bm.table(seqs[tt]);
       tables.insert(tables.end(), tb.begin(), tb.end());
+      tables.insert(tables.end(), kTableReserve, 0);
+      p.thread_table[tt] = tb;
+      p.thread_table_off[tt] = table_off[tt];
+      p.thread_table_cap[tt] = static_cast<int32_t>(tb.size()) + kTableReserve;
     }
+    const bool priv = rg.threads.size() == 1;
     for (int32_t h = 0; h < hkv; ++h) {
       ItemDesc it{};
       it.kv_head = h;
@@ -180,6 +199,10 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
       it.n_blocks = static_cast<int32_t>(bm.table(seqs[tt]).size());
       it.row_off = static_cast<int32_t>(rows.size());
       it.n_rows = range_rows[r];
+      it.hi = rg.hi;
+      it.grow = 0;
+      it.thread = priv ? tt : -1;
+      if (priv) p.thread_items[tt].push_back(static_cast<int32_t>(items.size()));
       for (int32_t t : rg.threads)
         for (int32_t q = 0; q < n_rows[t]; ++q)
           for (int32_t j = 0; j < gq; ++j)
@@ -369,14 +392,15 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     p.n_lists = p.grid;
   }
   int32_t partial = 0;
-  for (WaveDesc& w : waves) {
+  for (size_t u = 0; u < waves.size(); ++u) {
+    WaveDesc& w = waves[u];
     if (w.item < 0) continue;
-    // block-table span the bf16 kernel stages for this unit (1040 entries)
-    const int32_t tb0 = w.tok_lo / kTileTokens * kTileTokens;
-    const int32_t span_end = tb0 + (w.tok_hi - tb0 + kTileTokens - 1) / kTileTokens * kTileTokens + 16;
-    if (span_end / shape.block_size - tb0 / shape.block_size + 1 > 1040) return "internal: unit too long";
+    if (unit_table_span(w.tok_lo, w.tok_hi, shape.block_size) > kUnitTableEntries) return "internal: unit too long";
     w.partial = partial;
     partial += w.nrows;
+    // the last unit of a private range is the one later decode steps extend
+    const ItemDesc& it = items[w.item];
+    if (it.thread >= 0 && w.tok_hi == it.hi) p.open_units.push_back(static_cast<int32_t>(u));
   }
   p.n_units = static_cast<int32_t>(waves.size());
   p.n_partials = partial;
@@ -428,6 +452,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   put(p.off_merge_off, count.data(), count.size() * sizeof(int32_t));
   put(p.off_part_slot, part_slot.data(), part_slot.size() * sizeof(int32_t));
   put(p.off_wg_off, wg_off.data(), wg_off.size() * sizeof(int32_t));
+  p.grow.assign(n_threads, 0);
 
   // Control words: the list cursors and the cursor of the argmax units a
   // verify launch takes after its lists (persistent launches); then the

@@ -47,7 +47,18 @@ struct Plan {
   size_t off_ws_cursors = 0;   // byte offsets inside the workspace
   size_t off_ws_o = 0;
   size_t off_ws_ml = 0;
+  // What a later decode step needs to reuse the plan (spork_plan_advance):
+  std::vector<int32_t> seqs, len;              // each thread's sequence and its length when planned
+  std::vector<int32_t> grow;                   // tokens appended since, as last written into the image
+  std::vector<std::vector<int32_t>> thread_items;  // the items of each thread's private range
+  std::vector<std::vector<int32_t>> thread_table;  // each copied table as planned and patched since
+  std::vector<int32_t> thread_table_off;       // its offset in the image's table area, -1 if not copied
+  std::vector<int32_t> thread_table_cap;       // entries the image holds for it (planned + kTableReserve)
+  std::vector<int32_t> open_units;             // units that end where their private range ends
 };
+
+// Block-table entries the bf16 kernel stages for a unit [tok_lo, tok_hi).
+int32_t unit_table_span(int32_t tok_lo, int32_t tok_hi, int32_t block_size);
 
 // Returns "" on success, else an error message (nothing is built).
 std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int32_t* seqs,

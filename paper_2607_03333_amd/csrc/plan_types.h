@@ -20,10 +20,16 @@ struct WaveDesc {
 struct ItemDesc {
   int32_t kv_head;
   int32_t table_off;  // offset of the block table in the image's table area
-  int32_t n_blocks;   // valid entries of that table
+  int32_t n_blocks;   // valid entries of that table when the plan was made
   int32_t row_off;    // offset of the item's rows in the row area
   int32_t n_rows;
-  int32_t pad;
+  int32_t hi;         // end of the item's range when the plan was made
+  // Tokens appended to the item's thread since the plan was made (a private
+  // range reused by later decode steps; always 0 for shared ranges): the
+  // range's last unit ends `grow` tokens later, its rows' horizons move by
+  // `grow`, and its table holds the blocks of hi + grow tokens.
+  int32_t grow;
+  int32_t thread;     // the thread of a private range, -1 for a shared one
 };
 
 // One query row of an item: output index (query row * Hq + query head) and
@@ -45,5 +51,10 @@ constexpr int kMaxUnitTokens = 16384;
 constexpr int kMinPieceTokens = 512;
 constexpr int kUnitOverheadTokens = 256;
 constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, workgroups dealt round-robin
+// Block-table entries the image keeps free after each thread's table, for
+// the blocks later decode steps append (see spork_plan_advance).
+constexpr int kTableReserve = 64;
+// Block-table entries of one unit's slice that the bf16 kernel stages in LDS.
+constexpr int kUnitTableEntries = 1040;
 
 }  // namespace spork

@@ -147,6 +147,19 @@ class DeviceWorkload:
         self.steps.append(step)
         return step
 
+    def advance(self, step, index):
+        """Apply the scenario up to step ``index`` and reuse ``step``'s plan
+        for it (spork_plan_advance patches the device image); the step's
+        query rows take step ``index``'s Q. Returns the same Step object."""
+        st = self.wl.steps[index]
+        self.apply(st.ops_before)
+        spork.spork_plan_advance(step.plan, self.cache, step.image)
+        step.q.copy_(to_device(st.q, self.wl.dtype, self.device))
+        step.index = index
+        step.spec = st
+        step.info = spork.spork_plan_get_info(step.plan)
+        return step
+
     def prepare_all(self):
         return [self.prepare(i) for i in range(len(self.wl.steps))]
 

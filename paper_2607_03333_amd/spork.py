@@ -72,6 +72,7 @@ _SIGNATURES = {
     "spork_cache_destroy": (ctypes.c_int, [_p]),
     "spork_seq_new": (ctypes.c_int, [_p, _pi32]),
     "spork_seq_append": (ctypes.c_int, [_p, _c_i32, _c_i32, _p, _p, _pi32]),
+    "spork_seq_append_batch": (ctypes.c_int, [_p, _p, _p, _c_i32, _p, _p, _pi32]),
     "spork_fork": (ctypes.c_int, [_p, _c_i32, _pi32]),
     "spork_seq_free": (ctypes.c_int, [_p, _c_i32]),
     "spork_seq_len": (ctypes.c_int, [_p, _c_i32, _pi32]),
@@ -87,6 +88,7 @@ _SIGNATURES = {
     "spork_plan_destroy": (ctypes.c_int, [_p]),
     "spork_plan_get_info": (ctypes.c_int, [_p, ctypes.POINTER(spork_plan_info)]),
     "spork_plan_image": (ctypes.c_int, [_p, _p, ctypes.c_size_t]),
+    "spork_plan_advance": (ctypes.c_int, [_p, _p, _p, _p]),
     "spork_workspace_clear": (ctypes.c_int, [_p, _p, ctypes.c_size_t, _p]),
     "spork_attn_decode": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "spork_verify_workspace_bytes": (ctypes.c_int, [_c_i32, _c_i32, _c_i32,
@@ -192,6 +194,18 @@ def spork_seq_append(cache, seq, n_tokens):
     return slots[:n_tokens], ([tuple(int(x) for x in cow)] if n_cow.value else [])
 
 
+def spork_seq_append_batch(cache, seqs, n_tokens):
+    """Returns (slots int64 array in batch order, list of (src, dst, n_valid) copies)."""
+    seqs, n_tokens = _i32(seqs), _i32(n_tokens)
+    slots = np.zeros(max(int(np.maximum(n_tokens, 0).sum()), 1), dtype=np.int64)
+    cow = np.zeros(max(3 * len(seqs), 3), dtype=np.int32)
+    n_cow = _c_i32()
+    _check(lib().spork_seq_append_batch(cache, _ptr(seqs), _ptr(n_tokens), len(seqs), _ptr(slots), _ptr(cow),
+                                        ctypes.byref(n_cow)))
+    return slots[:int(np.maximum(n_tokens, 0).sum())], [tuple(int(x) for x in cow[3 * i:3 * i + 3])
+                                                        for i in range(n_cow.value)]
+
+
 def spork_fork(cache, parent_seq):
     c = _c_i32()
     _check(lib().spork_fork(cache, parent_seq, ctypes.byref(c)))
@@ -266,6 +280,10 @@ def spork_plan_get_info(plan):
     info = spork_plan_info()
     _check(lib().spork_plan_get_info(plan, ctypes.byref(info)))
     return {name: getattr(info, name) for name, _ in spork_plan_info._fields_}
+
+
+def spork_plan_advance(plan, cache, dev_image, stream=None):
+    _check(lib().spork_plan_advance(plan, cache, _ptr(dev_image), _stream(stream)))
 
 
 def spork_plan_image(plan):

@@ -693,3 +693,41 @@ def add_supersession_step(wl, more=(20, 120), own=(4, 30), seed=0):
     groups = [wl.thread(s).session for s in seqs]
     wl.steps.append(Step(seqs=seqs, n_rows=[1] * len(seqs), groups=groups, q=q, ops_before=ops))
     return wl
+
+
+def add_decode_steps(wl, n_steps, seed=0):
+    """``n_steps`` more steps after the workload's last one, as a decode loop
+    runs them: before each, every thread of the last step appends one token
+    (its K and V drawn from ``[42, 10, seed, step, seq]``); each step queries
+    the same threads with the same rows (the last ``n_rows`` positions of the
+    grown contexts) and fresh Q from ``default_rng([42, 10, seed])``. A verify
+    step's logits and drafts are kept, so its accept results stay the same.
+    The pool grows by enough blocks, appended at the back of the free order
+    (earlier allocations are unchanged).
+    Consecutive steps can therefore reuse one plan (spork_plan_advance)."""
+    rng = np.random.default_rng([42, 10, seed])
+    base = wl.steps[-1]
+    hkv, d, dtype = wl.hkv, wl.d, wl.dtype
+    # room in the pool for the new tokens: fresh block ids at the back of the free order
+    extra = len(base.seqs) * (-(-n_steps // wl.block_size) + 1)
+    wl.free_order = np.concatenate([wl.free_order, np.arange(wl.num_blocks, wl.num_blocks + extra, dtype=np.int32)])
+    wl.num_blocks += extra
+    for i in range(n_steps):
+        j = len(wl.steps)
+        ops = []
+        for seq in base.seqs:
+            key = [42, 10, seed, j, seq]
+            wl.kv_src[("s", seq)] = wl.kv_src[("s", seq)] + [(key, 1)]
+            wl._kv_cache.pop(("s", seq), None)
+            if wl.suffix_k is not None:
+                k, v = draw_kv(key, 1, hkv, d, dtype)
+                wl.suffix_k[seq] = np.concatenate([wl.suffix_k[seq], k])
+                wl.suffix_v[seq] = np.concatenate([wl.suffix_v[seq], v])
+            wl.thread(seq).suffix += 1
+            ops.append(("append", seq, 1))
+        q = to_storage(rng.standard_normal((sum(base.n_rows), wl.hq, d), dtype=np.float32), dtype)
+        wl.steps.append(Step(seqs=list(base.seqs), n_rows=list(base.n_rows), groups=list(base.groups), q=q,
+                             ops_before=ops, logits=base.logits, drafts=base.drafts,
+                             planted_greedy=base.planted_greedy, planted_accept=base.planted_accept,
+                             planted_next=base.planted_next, verify_k=base.verify_k))
+    return wl

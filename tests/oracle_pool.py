@@ -17,13 +17,22 @@ _LIMITS = None
 
 
 def build(case):
-    """The workload of a full-size case, without K/V arrays."""
+    """The workload of a full-size case, without K/V arrays. ``case`` is
+    (name, keyword arguments, supersede), optionally followed by a number of
+    decode steps (see decode_case)."""
     from paper_2607_03333_amd import synth
-    name, kw, supersede = case
+    name, kw, supersede = case[:3]
     wl = synth.make_named(name, kv=False, **kw)
     if supersede:
         wl = synth.add_supersession_step(wl)
+    if len(case) > 3 and case[3]:
+        synth.add_decode_steps(wl, case[3])
     return wl
+
+
+def decode_case(case, n_steps):
+    """The case followed by ``n_steps`` decode steps (synth.add_decode_steps)."""
+    return tuple(case[:3]) + (n_steps,)
 
 
 def _workload(case):

@@ -1,6 +1,7 @@
 """Host side of the C ABI, on the CPU: exports, block manager parity with the
 oracle (bit-exact tables, slots, copies, refcounts and free queue), error
 codes, and planner invariants."""
+import copy
 import ctypes
 import os
 import re
@@ -55,6 +56,30 @@ def _apply_both(ops, nb, bs, order):
                     continue
                 gs, gc = spork.spork_seq_append(c, s, op[2])
                 assert gs.tolist() == slots and gc == cow
+            elif kind == "batch":
+                # distinct live sequences; the oracle runs the appends one by
+                # one and is restored when one of them runs out of blocks
+                pairs, seen = [], set()
+                for i, n in op[1]:
+                    s = live[i % len(live)]
+                    if s not in seen:
+                        seen.add(s)
+                        pairs.append((s, n))
+                saved = copy.deepcopy(bm)
+                try:
+                    want_slots, want_cow = [], []
+                    for s, n in pairs:
+                        sl, cw = bm.append(s, n)
+                        want_slots += sl
+                        want_cow += cw
+                except oracle.NoBlocksError:
+                    bm = saved
+                    with pytest.raises(spork.SporkError) as ei:
+                        spork.spork_seq_append_batch(c, [s for s, _ in pairs], [n for _, n in pairs])
+                    assert ei.value.code == spork.SPORK_E_NOBLOCKS
+                else:
+                    gs, gc = spork.spork_seq_append_batch(c, [s for s, _ in pairs], [n for _, n in pairs])
+                    assert gs.tolist() == want_slots and gc == want_cow
             elif kind == "fork":
                 p = live[op[1] % len(live)]
                 assert spork.spork_fork(c, p) == bm.fork(p)
@@ -77,6 +102,7 @@ _op = st.one_of(
     st.tuples(st.just("append"), st.integers(0, 7), st.integers(0, 9)),
     st.tuples(st.just("fork"), st.integers(0, 7)),
     st.tuples(st.just("free"), st.integers(0, 7)),
+    st.tuples(st.just("batch"), st.lists(st.tuples(st.integers(0, 7), st.integers(0, 9)), max_size=4)),
 )
 
 
@@ -288,8 +314,8 @@ def _image_sections(info, img, n_out):
     nw, ni = info["n_units"], info["n_items"]
     waves = raw[: nw * 6].reshape(nw, 6)
     off = al(nw * 24)
-    items = raw[off: off + ni * 6].reshape(-1, 6)
-    off += al(ni * 24)
+    items = raw[off: off + ni * 8].reshape(-1, 8)
+    off += al(ni * 32)
     nrow = int(items[:, 4].sum())
     rows = raw[off: off + 2 * nrow].reshape(-1, 2)
     off += al(nrow * 8)
@@ -558,5 +584,68 @@ def test_supersession_plan():
     info = spork.spork_plan_get_info(p)
     assert info["unique_kv_bytes"] == wl.unique_kv_bytes(1)
     _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
+def _cache_for(wl, spare=0):
+    """A cache replaying the workload's scenario, with ``spare`` more free
+    blocks at the back of the free order."""
+    order = np.concatenate([wl.free_order, np.arange(wl.num_blocks, wl.num_blocks + spare, dtype=np.int32)])
+    c = spork.spork_cache_create(wl.num_blocks + spare, wl.block_size, order)
+    for stp in wl.steps:
+        for op in stp.ops_before:
+            {"new": lambda o: spork.spork_seq_new(c), "append": lambda o: spork.spork_seq_append(c, o[1], o[2]),
+             "fork": lambda o: spork.spork_fork(c, o[1]), "free": lambda o: spork.spork_seq_free(c, o[1])}[op[0]](op)
+    return c
+
+
+def test_plan_advance_refuses_what_it_cannot_absorb():
+    """spork_plan_advance checks everything before it launches: no growth is a
+    no-op; a freed sequence, a planned block replaced by copy-on-write, more
+    new blocks than the reserve, or a grown thread without a private range
+    are refused, with the plan left as it was."""
+    wl = synth.make(4, sessions=2, prefix=200, suffix=("uniform", 5, 40), vocab=300, kv=False)
+    stp = wl.steps[-1]
+    shape = spork.make_shape(wl.hq, wl.hkv, wl.d, wl.block_size, spork.SPORK_DTYPE_BF16, wl.sm_scale)
+    img_dev = 1 << 20    # a 256-aligned address; nothing is launched in this test
+
+    def fresh(spare=0):
+        c = _cache_for(wl, spare)
+        return c, spork.spork_plan_create(c, shape, stp.seqs, stp.n_rows, stp.groups, 8)
+
+    c, p = fresh()
+    before = spork.spork_plan_image(p).copy()
+    spork.spork_plan_advance(p, c, img_dev, stream=0)            # nothing grew: no-op
+    assert np.array_equal(spork.spork_plan_image(p), before)
+    spork.spork_seq_free(c, stp.seqs[1])
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_plan_advance(p, c, img_dev, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL and "freed" in str(e.value)
+    assert np.array_equal(spork.spork_plan_image(p), before)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+    c, p = fresh(spare=200)
+    main = stp.seqs[0]
+    if spork.spork_seq_len(c, main) % wl.block_size == 0:
+        spork.spork_seq_append(c, main, 1)                       # leave the last block partly filled
+        spork.spork_plan_destroy(p)
+        p = spork.spork_plan_create(c, shape, stp.seqs, stp.n_rows, stp.groups, 8)
+    before = spork.spork_plan_image(p).copy()
+    spork.spork_fork(c, main)                                    # shares the partial last block ...
+    spork.spork_seq_append(c, main, 1)                           # ... so this append copies it
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_plan_advance(p, c, img_dev, stream=0)
+    assert e.value.code == spork.SPORK_E_INVAL and "copy-on-write" in str(e.value)
+    assert np.array_equal(spork.spork_plan_image(p), before)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+    c, p = fresh(spare=200)
+    spork.spork_seq_append(c, stp.seqs[2], 65 * wl.block_size)   # 65 new blocks: one past the reserve
+    with pytest.raises(spork.SporkError) as e:
+        spork.spork_plan_advance(p, c, img_dev, stream=0)
+    assert e.value.code == spork.SPORK_E_CAPACITY and "reserve" in str(e.value)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)

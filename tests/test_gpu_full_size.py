@@ -91,3 +91,40 @@ def test_full_size_workload(case_id, pool):
             compare_attention(wl, step, tag=tag, ref=ref)
     finally:
         dw.close()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_decode_loop(pool):
+    """The bench workload, then 16 decode steps on one plan (every thread
+    appends a token per step; spork_plan_advance patches the image): every
+    thread of the last step against the oracle, and that step run twice bit
+    for bit."""
+    case = ("qwen3-30b-a3b-mixed", {}, False)
+    wl = synth.make_named(case[0])
+    synth.add_decode_steps(wl, 16)
+    dw = runner.DeviceWorkload(wl, poison_pool=True)
+    try:
+        step = dw.prepare(0)
+        units = step.info["n_units"]
+        for i in range(1, len(wl.steps)):
+            dw.advance(step, i)
+            step.run()
+        torch.cuda.synchronize()
+        assert step.info["n_units"] == units and int(dw.bad_slots.item()) == 0
+        last = len(wl.steps) - 1
+        futures = pool.submit(oracle_pool.decode_case(case, 16), wl, last)
+        tag = f"full decode loop step {last}"
+        step.poison()
+        step.run()
+        torch.cuda.synchronize()
+        first = snapshot(step)
+        compare_accept(wl, step, tag=tag)
+        step.poison()
+        step.run()
+        torch.cuda.synchronize()
+        assert_bit_equal(first, step, tag)
+        ref = {t: (row, o, lse) for f in futures for t, row, o, lse in f.result()}
+        assert sorted(ref) == list(range(len(step.spec.seqs)))
+        compare_attention(wl, step, tag=tag, ref=ref)
+    finally:
+        dw.close()
