@@ -21,7 +21,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
-HOST_SOURCES = ["block_manager.cpp", "plan.cpp", "capi.cpp"]
+HOST_SOURCES = ["block_manager.cpp", "plan.cpp", "capi.cpp", "dispatch_rules.cpp"]
 DEVICE_SOURCES = ["attention.hip", "vocab.hip", "kv.hip", "ngram.hip", "ceiling.hip", "noalloc.hip"]
 DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -849,6 +849,7 @@ AttnKernel pick_f32(int rt) {
   }
 }
 
+// Exactly the shapes attention_supported (dispatch_rules.cpp) accepts.
 AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt, int32_t waves) {
   if (dtype == 1 && d == 128 && (waves == 4 || waves == 8)) {
     if (bs == 16) return waves == 4 ? pick_bf16<16, 4>(rt) : pick_bf16<16, 8>(rt);
@@ -864,10 +865,6 @@ AttnKernel pick_attention(int32_t dtype, int32_t d, int32_t bs, int32_t rt, int3
 }
 
 }  // namespace
-
-bool attention_supported(int32_t dtype, int32_t head_dim, int32_t block_size, int32_t row_tiles, int32_t waves) {
-  return pick_attention(dtype, head_dim, block_size, row_tiles, waves) != nullptr;
-}
 
 hipError_t launch_attn_partial(const AttnArgs& a, hipStream_t stream) {
   AttnKernel k = pick_attention(a.dtype, a.head_dim, a.block_size, a.row_tiles, a.wg_waves);

@@ -83,11 +83,6 @@ __global__ void __launch_bounds__(64) ngram_drafts(NgramArgs a) {
 
 }  // namespace
 
-int32_t ngram_chunks(int64_t max_len) {
-  const int64_t c = (max_len + kNgramChunk - 1) / kNgramChunk;
-  return static_cast<int32_t>(c < 1 ? 1 : c);
-}
-
 hipError_t launch_ngram_scan(const NgramArgs& a, hipStream_t stream) {
   if (a.n_seqs == 0) return hipSuccess;
   hipLaunchKernelGGL(ngram_scan, dim3(a.n_seqs * a.n_chunks), dim3(256), 0, stream, a);

@@ -85,13 +85,6 @@ __global__ void __launch_bounds__(64) conf_final(ConfArgs a) {
 
 }  // namespace
 
-int32_t accept_chunks(int32_t rows, int32_t vocab) {
-  const int32_t max_chunks = vocab / (256 * 8 * 4) > 1 ? vocab / (256 * 8 * 4) : 1;
-  int32_t c = rows > 0 ? (2048 + rows - 1) / rows : 1;
-  if (c > max_chunks) c = max_chunks;
-  return c < 1 ? 1 : c;
-}
-
 hipError_t launch_argmax(const AcceptArgs& a, hipStream_t stream) {
   const int rows = a.n_verify * (a.k_drafts + 1);
   if (rows == 0) return hipSuccess;

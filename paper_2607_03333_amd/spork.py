@@ -14,6 +14,9 @@ import os
 import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspork.so")
+# The sanitizer test of the host code loads an AddressSanitizer/UBSan build of
+# the host sources instead (its kernel launches all fail); unset otherwise.
+_HOST_SANITIZER_LIB = os.environ.get("SPORK_HOST_SANITIZER_LIB")
 
 SPORK_OK = 0
 SPORK_E_INVAL = -1
@@ -116,10 +119,11 @@ def lib():
     """The loaded library; raises if it has not been built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+        path = _HOST_SANITIZER_LIB or LIB_PATH
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with "
                                "`python -m paper_2607_03333_amd.build` (there is no fallback)")
-        handle = ctypes.CDLL(LIB_PATH)
+        handle = ctypes.CDLL(path)
         for name, (res, args) in _SIGNATURES.items():
             fn = getattr(handle, name)
             fn.restype = res
