@@ -112,23 +112,46 @@ def read_ceiling(torch, spork, nbytes=2 << 30, reps=10):
             "all": results}
 
 
-def cpu_baseline(wl, step_specs, target_s):
+def cpu_baseline(wl, step_specs, target_s, single_core=False):
     """The oracle, untuned, on whole sessions of the same workload until about
-    ``target_s`` seconds of CPU work; GB/s on the same unique-KV accounting."""
-    import numpy as np
+    ``target_s`` seconds of CPU work (passes over all sessions repeat for a
+    workload that takes less); GB/s on the same unique-KV accounting. BLAS
+    runs on every core it sees, or on one with ``single_core``."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
+    with threadpool_limits(1 if single_core else None):
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return _cpu_baseline(wl, step_specs, target_s, threads)
+
+
+def _cpu_baseline(wl, step_specs, target_s, threads):
     import oracle
     from paper_2607_03333_amd import synth
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = 1
     per_tok = 2 * wl.hkv * wl.d * (2 if wl.dtype == synth.BF16 else 4)
     sessions = sorted({t.session for t in wl.threads})
     done, nbytes, rows, t0 = 0, 0, 0, time.perf_counter()
-    for s in sessions:
+    passes = 0
+    while True:
+        for s in sessions:
+            done, nbytes, rows = _oracle_session(wl, step_specs, s, per_tok, done, nbytes, rows, oracle, synth)
+            if time.perf_counter() - t0 >= target_s:
+                break
+        passes += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    what = (f"{done} of {len(sessions)} sessions" if done <= len(sessions)
+            else f"{done} session runs, {done / len(sessions):.1f} passes over all {len(sessions)} sessions")
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{what} ({rows} query rows, {nbytes} unique KV bytes) in {dt:.1f} s, float64 NumPy, "
+                      f"{os.cpu_count()} logical CPUs visible"}
+
+
+def _oracle_session(wl, step_specs, s, per_tok, done, nbytes, rows, oracle, synth):
+    """The oracle over one session's threads in every step: gather, attention,
+    argmax and accept. Returns the updated counts."""
+    if True:
         for si, st in step_specs:
             row = 0
             vrow = 0
@@ -150,13 +173,7 @@ def cpu_baseline(wl, step_specs, target_s):
                     vrow += 1
                 row += n
             nbytes += wl.prefix_len[s] * per_tok
-        done += 1
-        if time.perf_counter() - t0 >= target_s:
-            break
-    dt = time.perf_counter() - t0
-    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {len(sessions)} sessions ({rows} query rows, {nbytes} unique KV bytes) "
-                      f"in {dt:.1f} s, float64 NumPy, {os.cpu_count()} logical CPUs visible"}
+        return done + 1, nbytes, rows
 
 
 def confidence_bench(args, torch, spork, synth):
@@ -354,6 +371,34 @@ def decode_bench(args, torch, spork, synth, runner):
         sys.exit(1)
 
 
+def cpu_baseline_all(args):
+    """The oracle on every benchmark workload with every core, and on the
+    two smallest also on one core; one JSON line."""
+    import platform
+
+    from paper_2607_03333_amd import synth
+    cpu = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu)
+    except OSError:
+        pass
+    res = []
+    for i, cfg in enumerate(synth.CONFIGS):
+        wl = synth.make(i)
+        specs = [(j, st) for j, st in enumerate(wl.steps)]
+        for single in ((False, True) if i <= 1 else (False,)):
+            r = cpu_baseline(wl, specs, args.cpu_seconds, single_core=single)
+            r["workload"] = cfg["name"]
+            res.append(r)
+            print(f"# {cfg['name']} {'1 core' if single else 'all cores'}: {r['value']:.4f} GB/s ({r['sample']})",
+                  file=sys.stderr, flush=True)
+        del wl
+    print(json.dumps({"metric": "oracle unique-KV GB/s on the host", "cpu": cpu,
+                      "logical_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+                      "results": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -364,6 +409,9 @@ def main():
                     help="draft length of the verify workloads (default: the workload's own)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-baseline-all", action="store_true",
+                    help="instead of the benchmark, time the oracle on the host for every workload (all cores, "
+                         "and one core for the two smallest) and exit; no GPU is used")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="instead of the benchmark, run one plain device copy of this many MiB "
                          "(reference kernel for the HBM traffic counters) and exit")
@@ -383,6 +431,10 @@ def main():
         print(json.dumps({"error": "this benchmark runs on one GPU only: the forked-decode path is "
                                    "measured on a single MI355X; --gpus must be 1"}), flush=True)
         sys.exit(2)
+
+    if args.cpu_baseline_all:
+        cpu_baseline_all(args)
+        return
 
     import torch
     from paper_2607_03333_amd import runner, spork, synth
