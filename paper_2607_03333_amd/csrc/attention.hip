@@ -6,11 +6,14 @@
 //    (Section 4.1: probes reuse the main thread's prefix KV), or one
 //    thread's private range, where verify rows apply the causal rule over
 //    the drafts (Section 4.3). Q.K^T and P.V run on MFMA with fp32
-//    accumulation; K and V stream from HBM with 16-byte loads straight into
-//    the MFMA operand registers.
-//  * merge: log-sum-exp merge of an output row's partials (DPP wave
-//    reductions), written in the input dtype, plus the row's lse; the same
-//    launch runs the accept of a verify step (Section 4.3, steps 2-3).
+//    accumulation. bf16: K and V stream from HBM with 16-byte direct-to-LDS
+//    loads (non-temporal) into a ring of LDS stages that the waves of a
+//    workgroup share; fp32: 16-byte loads straight into registers.
+//  * merge: log-sum-exp merge of an output row's partials (the batch's
+//    maximum and weighted sum by DPP reductions over eight lanes), written
+//    in the input dtype, plus the row's lse; the same launch runs the accept
+//    of a verify step (Section 4.3, steps 2-3) and clears the persistent
+//    launch's cursors for the next call.
 #include "device_common.h"
 
 namespace spork {
@@ -735,11 +738,12 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 //   M = max m_i, L = sum 2^(m_i - M) l_i, O = sum 2^(m_i - M) o_i / L,
 //   lse = (M + log2 L) ln 2. Partials with nothing visible (m = -inf, l = 0)
 //   add nothing.
-// Partials go in batches of 4 (outputs with at most 4) or 8: the batch's
-// partial ids come with one vector load (lane i: entry i), then the (m, l)
-// pairs and all output rows are loaded together, so a batch costs two memory
-// round trips whatever its size; unused slots repeat a valid id with weight
-// 0. Batches after the first rescale the running sums to the new maximum.
+// Partials go in batches of 4 (outputs with at most 4) or 8. An output's
+// partials are consecutive rows; lane i loads the (m, l) pair of partial i
+// and every lane its channels of all the batch's rows, in one round trip.
+// The batch maximum and the weighted sum of l are DPP reductions over lanes
+// 0-7; unused slots repeat a valid row with weight 0. Batches after the
+// first rescale the running sums to the new maximum.
 // --------------------------------------------------------------------------
 // One batch of at most B partials (entries c0 .. c0 + k - 1 of the output's
 // list), folded into the running (max, sum, accumulator).
@@ -760,10 +764,7 @@ __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bo
   const bool live = lane < k;
   const float pm = live ? ml.x : kNegInf;
   const float pl = live ? ml.y : 0.0f;
-  float bm = kNegInf;
-#pragma unroll
-  for (int i = 0; i < B; ++i)
-    bm = fmaxf(bm, __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pm), i)));
+  const float bm = lanes8_max(pm);  // lanes k.. hold -inf
   const float new_max = fmaxf(run_max, bm);
   const float new_mu = new_max == kNegInf ? 0.0f : new_max;
   if (!first) {
@@ -774,12 +775,11 @@ __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bo
   }
   run_max = new_max;
   mu = new_mu;
+  const float w = exp2_fast(pm - mu);  // lane i: weight of partial i, 0 for unused slots (pm = -inf)
+  sum += lanes8_sum(w * pl);
 #pragma unroll
   for (int i = 0; i < B; ++i) {
-    const float mi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pm), i));
-    const float li = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pl), i));
-    const float wgt = exp2_fast(mi - mu);  // 0 for unused slots (mi = -inf)
-    sum += wgt * li;
+    const float wgt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] += wgt * po[i][e];
   }

@@ -1,6 +1,7 @@
 // Device helpers shared by the gfx950 kernels: vector types, the fast
-// base-2 exponential, DPP wave reductions, and the accept of a verify thread
-// (run by the accept kernel and inside the merge launch).
+// base-2 exponential, DPP reductions over eight lanes, the greedy argmax of a
+// vocabulary chunk, and the accept of a verify thread (run by the accept
+// kernel and inside the merge launch).
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -25,33 +26,30 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // --------------------------------------------------------------------------
-// Wave-wide reductions with DPP: butterflies inside each 16-lane row
-// (quad permutes, half-row and row mirrors), then the row broadcasts 15 and
-// 31 carry the partial results across rows; lane 63 ends with the total.
+// Reductions over lanes 0-7 of a wave with DPP lane moves (no LDS round
+// trip): the quad permutes [1,0,3,2] and [2,3,0,1] combine each group of four
+// lanes, the half-row mirror (lane i <-> 7 - i inside each eight) combines
+// the two groups; lane 0 then holds the result over lanes 0-7, read out as a
+// wave-uniform value. Every lane of the wave must be active.
 // --------------------------------------------------------------------------
-template <int kCtrl, int kRowMask>
-__device__ __forceinline__ float dpp_mov(float ident, float x) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, ident), __builtin_bit_cast(int, x),
-                                         kCtrl, kRowMask, 0xF, false));
+template <int kCtrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), kCtrl, 0xF, 0xF, false));
 }
 
 template <typename Op>
-__device__ __forceinline__ float wave_reduce(float x, float ident, Op op) {
-  x = op(x, dpp_mov<0xB1, 0xF>(ident, x));   // quad_perm [1,0,3,2]
-  x = op(x, dpp_mov<0x4E, 0xF>(ident, x));   // quad_perm [2,3,0,1]
-  x = op(x, dpp_mov<0x141, 0xF>(ident, x));  // row_half_mirror
-  x = op(x, dpp_mov<0x140, 0xF>(ident, x));  // row_mirror
-  x = op(x, dpp_mov<0x142, 0xA>(ident, x));  // row_bcast:15 into rows 1 and 3
-  x = op(x, dpp_mov<0x143, 0xC>(ident, x));  // row_bcast:31 into rows 2 and 3
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
+__device__ __forceinline__ float lanes8_reduce(float x, Op op) {
+  x = op(x, dpp_mov<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = op(x, dpp_mov<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = op(x, dpp_mov<0x141>(x));  // row_half_mirror
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-  return wave_reduce(x, kNegInf, [](float a, float b) { return fmaxf(a, b); });
+__device__ __forceinline__ float lanes8_max(float x) {
+  return lanes8_reduce(x, [](float a, float b) { return fmaxf(a, b); });
 }
-__device__ __forceinline__ float wave_sum(float x) {
-  return wave_reduce(x, 0.0f, [](float a, float b) { return a + b; });
+__device__ __forceinline__ float lanes8_sum(float x) {
+  return lanes8_reduce(x, [](float a, float b) { return a + b; });
 }
 
 __device__ __forceinline__ int wave_min_int(int x) {
