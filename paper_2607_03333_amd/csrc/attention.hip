@@ -136,12 +136,24 @@ __device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
   return r;
 }
 
-// One dword from LDS at a wave-uniform address, returned in an SGPR.
-__device__ __forceinline__ int lds_read_uniform_i32(uint32_t addr) {
-  int r;
-  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(addr) : "memory");
-  return __builtin_amdgcn_readfirstlane(r);
+// The block-table entries of one stage, read from LDS at a wave-uniform
+// address without a wait: two adjacent entries (16-token blocks, one per half
+// of the stage) or one (32-token blocks). tab_wait() waits for the read and
+// takes the registers as in-out operands, so no use moves above it.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+template <int BS>
+__device__ __forceinline__ u32x2 tab_read(uint32_t addr) {
+  u32x2 r;
+  if constexpr (BS == 16) {
+    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+  } else {
+    uint32_t x;
+    asm volatile("ds_read_b32 %0, %1" : "=v"(x) : "v"(addr) : "memory");
+    r = u32x2{x, x};
+  }
+  return r;
 }
+__device__ __forceinline__ void tab_wait(u32x2& r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r) : : "memory"); }
 
 template <int N>
 __device__ __forceinline__ void lds_wait(u32x4 (&r)[N]) {
@@ -194,7 +206,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   static_assert(BS == 16 || BS == 32, "unsupported block size");
   static_assert(NW == 4 || NW == 8, "workgroups of 4 or 8 waves");
   __shared__ uint4 smem[kRing][kStageChunks];
-  __shared__ int tab[kUnitBlocks];
+  __shared__ __align__(16) int tab[kUnitBlocks];
   __shared__ int next_unit;
   // Persistent workgroup: it takes the next unit of its compute unit's list
   // (shared with the other workgroup resident there) until the list is done.
@@ -301,10 +313,11 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   }
   const uint16_t* pool = wave < NW / 2 ? kc : vc;
   // The unit's slice of the block table, staged in LDS before the ring
-  // starts (tab[i] = table entry tb0/BS + i, clamped to the table) and read
-  // per stage outside the compiler's view (a vector load of the table inside
-  // the loop would make its wait also wait for every direct-to-LDS load
-  // issued before it).
+  // starts (tab[i] = table entry tb0/BS + i, clamped to the table; stage st
+  // uses entries 2*st and 2*st + 1 with 16-token blocks, st with 32-token
+  // ones) and read per stage outside the compiler's view (a vector load of
+  // the table inside the loop would make its wait also wait for every
+  // direct-to-LDS load issued before it), one stage ahead of its use.
   const int tab0 = tb0 / BS;
   const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
   for (int i = tid; i < ntab; i += NT_) {
@@ -312,11 +325,18 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     tab[i] = table[bi < nb ? bi : nb - 1];
   }
   __syncthreads();
-  // Issue the direct-to-LDS loads of stage `st` into ring slot st % kRing.
-  auto issue_stage = [&](int st) __attribute__((always_inline)) {
-    const int tb = tb0 + st * kTileTokens;
-    const int e0 = lds_read_uniform_i32(lds_addr(&tab[tb / BS - tab0]));
-    const int e1 = lds_read_uniform_i32(lds_addr(&tab[(tb + 16) / BS - tab0]));
+  // Table entries of stage `st` (clamped to the unit's last stage), read
+  // without a wait.
+  const uint32_t tab_base = lds_addr(&tab[0]);
+  auto stage_entries = [&](int st) __attribute__((always_inline)) {
+    const int s = min(st, nstage - 1);
+    return tab_read<BS>(tab_base + 4u * static_cast<uint32_t>(BS == 16 ? 2 * s : s));
+  };
+  // Issue the direct-to-LDS loads of stage `st` into ring slot st % kRing,
+  // `ent` holding its table entries (already waited for).
+  auto issue_stage = [&](int st, const u32x2& ent) __attribute__((always_inline)) {
+    const int e0 = __builtin_amdgcn_readfirstlane(static_cast<int>(ent.x));
+    const int e1 = __builtin_amdgcn_readfirstlane(static_cast<int>(ent.y));
     const size_t base0 = (static_cast<size_t>(e0) * hkv + head) * (static_cast<size_t>(BS) * D);
     const size_t base1 = (static_cast<size_t>(e1) * hkv + head) * (static_cast<size_t>(BS) * D);
     uint4* slot = smem[st % kRing];
@@ -514,19 +534,32 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   wait_vmcnt<0>();
   // Prologue: stages 0 .. kRing-2 in flight.
 #pragma unroll
-  for (int st = 0; st < kRing - 1; ++st)
-    if (st < nstage) issue_stage(st);
+  for (int st = 0; st < kRing - 1; ++st) {
+    if (st < nstage) {
+      u32x2 ent = stage_entries(st);
+      tab_wait(ent);
+      issue_stage(st, ent);
+    }
+  }
 
   // The ring loop, specialised on the number of tiles this wave owns so that
   // no branch on it sits inside the loop. Every wave runs nstage barriers.
   auto run = [&](auto nt_c) __attribute__((always_inline)) {
     constexpr int NT = decltype(nt_c)::value;
+    // Table entries of the stage the next iteration issues, read one
+    // iteration ahead: the operand waits of this iteration's compute cover
+    // their latency.
+    u32x2 ent = stage_entries(kRing - 1);
     for (int st = 0; st < nstage; ++st) {
       // Wait for this wave's loads of stage st: the stages issued after it
       // (at most kRing - 2 of them, LPW loads each) may stay in flight.
       wait_stage<kRing, LPW>(min(kRing - 2, nstage - 1 - st));
       barrier_nofence();  // stage st visible to all waves; slot of stage st-1 free
-      if (st + kRing - 1 < nstage) issue_stage(st + kRing - 1);
+      if (st + kRing - 1 < nstage) {
+        tab_wait(ent);
+        issue_stage(st + kRing - 1, ent);
+      }
+      ent = stage_entries(st + kRing);
       if constexpr (NT > 0) compute_tiles(nt_c, st);
     }
     wait_vmcnt<0>();
