@@ -59,7 +59,7 @@ def check(logits, dtype, span_off, theta=THETA, tag=""):
     err_c = float(np.max(np.abs(conf - want_c))) if len(conf) else 0.0
     say(f"  {tag}: rows {x.shape[0]} vocab {x.shape[1]} probes {len(span_off) - 1} "
         f"max|dl| {err_l:.2e} max|dc| {err_c:.2e} commits {int(commit.sum())}")
-    assert np.array_equal(am, np.argmax(x, axis=1))
+    assert np.array_equal(am, oracle.argmax_rows(x))
     assert err_l <= LOGPROB_TOL and err_c <= LOGPROB_TOL
     far = np.abs(want_c - theta) > LOGPROB_TOL
     assert np.array_equal(commit[far].astype(bool), want_g[far])

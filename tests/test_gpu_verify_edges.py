@@ -2,9 +2,11 @@
 
 Through the C ABI: an accept-only call with no drafts (K = 0: the step
 commits the greedy token of the one row), drafts longer than a wave (K = 100,
-first mismatches past lane 63 and an all-match), and the argmax inside the
-persistent attention launch on a vocabulary that is not a multiple of the
-16-byte vector (the scalar scan path).
+first mismatches past lane 63 and an all-match), the argmax over the full
+151,936-entry vocabulary on maxima held by +0 and -0, natural (unplanted)
+ties of coarsely rounded, saturating logits, a tie at the last two entries and an all -inf
+row, and the argmax inside the persistent attention launch on a vocabulary
+that is not a multiple of the 16-byte vector (the scalar scan path).
 """
 import numpy as np
 import pytest
@@ -67,6 +69,35 @@ def test_drafts_longer_than_a_wave():
             d[s, m] = (g[s, m] + 1) % vocab
     a = check(synth.to_storage(x, synth.BF16), synth.BF16, d, "K=100")
     assert a.tolist() == [70, 99, 100, 63]
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
+def test_argmax_signed_zeros_and_natural_ties_full_vocabulary(dtype):
+    # -0 and +0 compare equal, so a maximum held by both goes to the lower
+    # index whichever sign it has
+    vocab, n, k = 151936, 3, 3
+    rng = np.random.default_rng(11)
+    x = -np.abs(rng.standard_normal((n * (k + 1), vocab)).astype(np.float32)) - 1.0
+    x[0, 100], x[0, 5000] = -0.0, 0.0          # -0 first
+    x[1, 3], x[1, 7] = 0.0, -0.0               # +0 first
+    x[2, :] = -0.0
+    x[2, 151000] = 0.0                         # every entry a zero: index 0
+    x[3] = np.minimum(np.round(rng.standard_normal(vocab)), 3.0)   # coarse, saturating: the maximum repeats
+    x[4, vocab - 2], x[4, vocab - 1] = 3.0, 3.0                # tie at the last two entries
+    x[5, :] = -np.inf                          # nothing finite: index 0
+    x[6] = np.minimum(np.round(rng.standard_normal(vocab) * 8.0) / 8.0, 2.0)
+    x[7] = rng.standard_normal(vocab).astype(np.float32)
+    st = synth.to_storage(x, dtype)
+    xs = synth.to_f64(st, dtype)
+    natural = [int((xs[r] == xs[r].max()).sum()) for r in (3, 6)]
+    assert min(natural) > 1, natural            # the coarse rows do tie at the maximum
+    assert np.signbit(xs[0, 100]) and not np.signbit(xs[0, 5000]) and np.signbit(xs[1, 7])
+    g = oracle.argmax_rows(xs).reshape(n, k + 1)
+    assert g[0, 0] == 100 and g[0, 1] == 3 and g[0, 2] == 0 and g[1, 0] == vocab - 2 and g[1, 1] == 0
+    drafts = g[:, :k].copy()
+    drafts[1, 2] = (g[1, 2] + 1) % vocab       # thread 1 stops at its third draft
+    a = check(st, dtype, drafts, f"signed zeros and ties {dtype} V={vocab}")
+    assert a.tolist() == [3, 2, 3]
 
 
 def test_argmax_in_the_attention_tail_on_a_ragged_vocabulary():
