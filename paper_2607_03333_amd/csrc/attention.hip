@@ -248,18 +248,16 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   // Query operands, row horizons and partial-result positions of this
   // wave's tiles.
   bf16x8 qop[RTW][4];
-  int hz[RTW], slot[RTW];
+  int hz[RTW];
   bool own[RTW];
 #pragma unroll
   for (int j = 0; j < RTW; ++j) {
     const int tile = cw + NW * j;
     own[j] = tile < ntiles;
     const int i = tile * 16 + r16;
-    slot[j] = 0;
     if (own[j] && i < w.nrows) {
       const RowDesc rd = a.rows[it.row_off + w.row0 + i];
       hz[j] = rd.horizon + grow;
-      slot[j] = a.part_slot[w.partial + i];
       const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rd.qidx) * D);
 #pragma unroll
       for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(qp[4 * s + g]);
@@ -354,17 +352,18 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   //     chunk t*16 + ((4s + g) ^ fk(t));
   //   V operand (channel tile dt): chunk 512 + 4*(16*dt + r16) + (g ^ ((r16 >> 1) & 3)),
   //     i.e. a per-lane base plus 1024 bytes per dt.
-  uint32_t kaddr[8];
+  //   The second half's token is the first half's plus 4 with the same
+  //   swizzle, so its addresses are the first half's plus 1024 bytes.
+  uint32_t kaddr[4];
+  {
+    const int t = 8 * (r16 >> 2) + (r16 & 3);
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int t = 8 * (r16 >> 2) + 4 * hh + (r16 & 3);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) kaddr[4 * hh + s] = 16u * (t * 16 + ((4 * s + g) ^ k_swz(t)));
+    for (int s = 0; s < 4; ++s) kaddr[s] = 16u * (t * 16 + ((4 * s + g) ^ k_swz(t)));
   }
   const uint32_t smem_base = lds_addr(&smem[0][0]);
   const uint32_t vaddr = smem_base + 16u * (512 + 4 * r16 + (g ^ ((r16 >> 1) & 3)));
 #pragma unroll
-  for (int i = 0; i < 8; ++i) kaddr[i] += smem_base;
+  for (int i = 0; i < 4; ++i) kaddr[i] += smem_base;
 
   // Softmax in base 2 with a lazily moved reference max: scores enter as
   // p = 2^(s*c - m) with m the row's reference; m (and the accumulator, by
@@ -381,7 +380,9 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     const bool edge = tb < w.tok_lo || tb + kTileTokens > tok_hi || tb + kTileTokens - 1 > hmin;
     u32x4 kr[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) kr[i] = lds_read_b128(kaddr[i] + soff);
+    for (int i = 0; i < 4; ++i) kr[i] = lds_read_b128(kaddr[i] + soff);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kr[4 + i] = lds_read_b128<1024>(kaddr[i] + soff);
     lds_wait(kr);
     f32x4 sc[NT][2];
 #pragma unroll
@@ -569,7 +570,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
       lt += __shfl_xor(lt, 32);
       const int i = (cw + NW * j) * 16 + r16;
       if (i < w.nrows) {
-        const size_t pr = static_cast<size_t>(slot[j]);
+        const size_t pr = static_cast<size_t>(a.part_slot[w.partial + i]);
         if (g == 0) {
           a.part_ml[2 * pr] = m[j];
           a.part_ml[2 * pr + 1] = lt;
