@@ -85,9 +85,9 @@ constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 by
 template <int NW>
 constexpr int ring_of() { return NW == 4 ? 4 : 8; }
 
-// Wait until at most `after` stages of this wave's direct-to-LDS loads (LPW
-// per stage) are still in flight.
-template <int RING, int LPW>
+// Wait until at most `after` (0..7) stages of this wave's direct-to-LDS
+// loads (LPW per stage), and no older vector load, are still in flight.
+template <int LPW>
 __device__ __forceinline__ void wait_stage(int after);
 // Cache-policy bits of the K/V loads: non-temporal. Every KV byte is read
 // once per launch, and streaming loads marked this way reach 7.2 TB/s on
@@ -165,6 +165,42 @@ __device__ __forceinline__ void lds_wait(u32x4 (&r)[N]) {
                : "memory");
 }
 
+// Workgroup-uniform reads of a unit's descriptors from the plan image (which
+// no kernel writes while the attention launch runs) as scalar loads, on the
+// scalar cache and its own counter, instead of vector loads that queue behind
+// the stream's loads. Exactly the descriptor's bytes are read.
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ WaveDesc load_wave_desc(const WaveDesc* p) {
+  static_assert(sizeof(WaveDesc) == 24, "WaveDesc layout");
+  i32x4 x;
+  i32x2 y;
+  asm volatile("s_load_dwordx4 %0, %2, 0x0\n\ts_load_dwordx2 %1, %2, 0x10\n\ts_waitcnt lgkmcnt(0)"
+               : "=s"(x), "=s"(y)
+               : "s"(p)
+               : "memory");
+  return WaveDesc{x[0], x[1], x[2], x[3], y[0], y[1]};
+}
+__device__ __forceinline__ ItemDesc load_item_desc(const ItemDesc* p) {
+  static_assert(sizeof(ItemDesc) == 32, "ItemDesc layout");
+  i32x8 x;
+  asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(x) : "s"(p) : "memory");
+  ItemDesc it;
+  static_assert(sizeof(it) == sizeof(x), "ItemDesc layout");
+  __builtin_memcpy(&it, &x, sizeof(it));
+  return it;
+}
+__device__ __forceinline__ int load_int_uniform(const int32_t* p) {
+  int x;
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(x) : "s"(p) : "memory");
+  return x;
+}
+
+// Workgroup barrier that publishes this wave's LDS writes (and no global
+// memory operation: no fence).
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Workgroup barrier without the memory fence of __syncthreads(): callers make
 // their own direct-to-LDS loads complete first (wait_vmcnt). The memory
 // clobber keeps loads, stores and LDS operations on their side of it.
@@ -177,23 +213,18 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int RING, int LPW>
+template <int LPW>
 __device__ __forceinline__ void wait_stage(int after) {
-  if constexpr (RING == 4 && LPW == 4) {
-    if (after >= 2) wait_vmcnt<8>();
-    else if (after == 1) wait_vmcnt<4>();
-    else wait_vmcnt<0>();
-  } else {
-    static_assert(RING == 8 && LPW == 2, "ring shapes with a wait ladder");
-    switch (after) {
-      case 6: wait_vmcnt<12>(); break;
-      case 5: wait_vmcnt<10>(); break;
-      case 4: wait_vmcnt<8>(); break;
-      case 3: wait_vmcnt<6>(); break;
-      case 2: wait_vmcnt<4>(); break;
-      case 1: wait_vmcnt<2>(); break;
-      default: wait_vmcnt<0>(); break;
-    }
+  static_assert(7 * LPW < 64, "vmcnt range");
+  switch (after) {
+    case 7: wait_vmcnt<7 * LPW>(); break;
+    case 6: wait_vmcnt<6 * LPW>(); break;
+    case 5: wait_vmcnt<5 * LPW>(); break;
+    case 4: wait_vmcnt<4 * LPW>(); break;
+    case 3: wait_vmcnt<3 * LPW>(); break;
+    case 2: wait_vmcnt<2 * LPW>(); break;
+    case 1: wait_vmcnt<LPW>(); break;
+    default: wait_vmcnt<0>(); break;
   }
 }
 
@@ -212,18 +243,23 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   // (shared with the other workgroup resident there) until the list is done.
   const int tid = threadIdx.x;
   const int list = static_cast<int>(blockIdx.x) % a.n_lists;
-  const int list0 = a.wg_off[list], list_len = a.wg_off[list + 1] - list0;
-  for (;;) {
+  const int list0 = load_int_uniform(a.wg_off + list), list_len = load_int_uniform(a.wg_off + list + 1) - list0;
+  // Thread 0 takes each unit before the workgroup needs it: the first here,
+  // each next one at the end of the current unit, before its partial results
+  // are stored, so neither the atomic's round trip nor the stores' sit
+  // between two units. A barrier without a memory fence publishes the take.
   if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
-  __syncthreads();
+  for (;;) {
+  barrier_lds();
   const int taken = __builtin_amdgcn_readfirstlane(next_unit);
   if (taken < 0 || taken >= list_len) break;
-  const WaveDesc w = a.waves[list0 + taken];
+  const WaveDesc w = load_wave_desc(a.waves + list0 + taken);
   if (w.item < 0) {  // padding (not emitted on persistent lists): every wave reads next_unit first
-    __syncthreads();
+    barrier_nofence();
+    if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
     continue;
   }
-  const ItemDesc it = a.items[w.item];
+  const ItemDesc it = load_item_desc(a.items + w.item);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   // Row tiles go to waves by `cw`, the wave index rotated by two in the
   // second workgroup of a compute unit (workgroups b and b + n_lists share
@@ -245,27 +281,47 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   const size_t hkv = static_cast<size_t>(a.hkv);
   const int ntiles = (w.nrows + 15) >> 4;
 
-  // Query operands, row horizons and partial-result positions of this
-  // wave's tiles.
-  bf16x8 qop[RTW][4];
-  int hz[RTW];
-  bool own[RTW];
+  const int tb0 = w.tok_lo & ~(kTileTokens - 1);
+  const int nstage = (tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
+
+  // Row descriptors of this wave's tiles, loaded together with the unit's
+  // block table (below); the query rows they name are loaded once the table
+  // is staged, and complete behind the ring's first loads.
+  RowDesc rdesc[RTW];
+  bool own[RTW], has_row[RTW];
 #pragma unroll
   for (int j = 0; j < RTW; ++j) {
     const int tile = cw + NW * j;
     own[j] = tile < ntiles;
     const int i = tile * 16 + r16;
-    if (own[j] && i < w.nrows) {
-      const RowDesc rd = a.rows[it.row_off + w.row0 + i];
-      hz[j] = rd.horizon + grow;
-      const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rd.qidx) * D);
+    has_row[j] = own[j] && i < w.nrows;
+    rdesc[j] = a.rows[it.row_off + w.row0 + (has_row[j] ? i : 0)];  // padding lanes: the unit's first row, unused
+  }
+  // The unit's slice of the block table, staged in LDS before the ring
+  // starts (tab[i] = table entry tb0/BS + i, clamped to the table; stage st
+  // uses entries 2*st and 2*st + 1 with 16-token blocks, st with 32-token
+  // ones) and read per stage outside the compiler's view (a vector load of
+  // the table inside the loop would make its wait also wait for every
+  // direct-to-LDS load issued before it), one stage ahead of its use.
+  const int tab0 = tb0 / BS;
+  const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
+  for (int i = tid; i < ntab; i += NT_) {
+    const int bi = tab0 + i;
+    tab[i] = table[bi < nb ? bi : nb - 1];
+  }
+
+  // Query operands and row horizons of this wave's tiles. A padding lane
+  // (past the slice's rows) computes on the unit's first row with no causal
+  // limit and is never stored; loading it like the others keeps the query
+  // loads free of branches, whose merges would wait for them here.
+  bf16x8 qop[RTW][4];
+  int hz[RTW];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(qp[4 * s + g]);
-    } else {
-      hz[j] = INT_MAX;  // padding row: zero query, never written
+  for (int j = 0; j < RTW; ++j) {
+    hz[j] = has_row[j] ? rdesc[j].horizon + grow : INT_MAX;
+    const uint4* qp = reinterpret_cast<const uint4*>(qg + static_cast<size_t>(rdesc[j].qidx) * D);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(make_uint4(0, 0, 0, 0));
-    }
+    for (int s = 0; s < 4; ++s) qop[j][s] = as_bf16x8(qp[4 * s + g]);
   }
   int hmin = INT_MAX;
 #pragma unroll
@@ -284,9 +340,6 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-
-  const int tb0 = w.tok_lo & ~(kTileTokens - 1);
-  const int nstage = (tok_hi - tb0 + kTileTokens - 1) / kTileTokens;
 
   // This lane's 4 chunks of a stage: instruction k of wave w fills chunks
   // (4w + k)*64 + lane. Waves 0-1: K chunks (token t, channel group c);
@@ -310,19 +363,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     }
   }
   const uint16_t* pool = wave < NW / 2 ? kc : vc;
-  // The unit's slice of the block table, staged in LDS before the ring
-  // starts (tab[i] = table entry tb0/BS + i, clamped to the table; stage st
-  // uses entries 2*st and 2*st + 1 with 16-token blocks, st with 32-token
-  // ones) and read per stage outside the compiler's view (a vector load of
-  // the table inside the loop would make its wait also wait for every
-  // direct-to-LDS load issued before it), one stage ahead of its use.
-  const int tab0 = tb0 / BS;
-  const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
-  for (int i = tid; i < ntab; i += NT_) {
-    const int bi = tab0 + i;
-    tab[i] = table[bi < nb ? bi : nb - 1];
-  }
-  __syncthreads();
+  barrier_lds();  // the table is in LDS; the query loads may still be in flight
   // Table entries of stage `st` (clamped to the unit's last stage), read
   // without a wait.
   const uint32_t tab_base = lds_addr(&tab[0]);
@@ -530,10 +571,10 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     }
   };
 
-  // Everything loaded so far (query rows) completes before the ring starts,
-  // so no wait for it lands inside the loop.
-  wait_vmcnt<0>();
-  // Prologue: stages 0 .. kRing-2 in flight.
+  // Prologue: stages 0 .. kRing-2 in flight. The query rows, loaded before
+  // them, complete first (vector loads complete in order): this wait leaves
+  // only the prologue's loads in flight, and no wait for the query rows
+  // lands inside the loop.
 #pragma unroll
   for (int st = 0; st < kRing - 1; ++st) {
     if (st < nstage) {
@@ -542,6 +583,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
       issue_stage(st, ent);
     }
   }
+  wait_stage<LPW>(min(kRing - 1, nstage));
 
   // The ring loop, specialised on the number of tiles this wave owns so that
   // no branch on it sits inside the loop. Every wave runs nstage barriers.
@@ -554,7 +596,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     for (int st = 0; st < nstage; ++st) {
       // Wait for this wave's loads of stage st: the stages issued after it
       // (at most kRing - 2 of them, LPW loads each) may stay in flight.
-      wait_stage<kRing, LPW>(min(kRing - 2, nstage - 1 - st));
+      wait_stage<LPW>(min(kRing - 2, nstage - 1 - st));
       barrier_nofence();  // stage st visible to all waves; slot of stage st-1 free
       if (st + kRing - 1 < nstage) {
         tab_wait(ent);
@@ -564,6 +606,10 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
       if constexpr (NT > 0) compute_tiles(nt_c, st);
     }
     wait_vmcnt<0>();
+    // Every wave has read this unit's take (the ring loop's barriers follow
+    // it): take the next unit now.
+    int nxt = 0;
+    if (tid == 0) nxt = atomicAdd(a.cursors + list, 1);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       float lt = l[j] + __shfl_xor(l[j], 16);
@@ -580,6 +626,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
           *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[j][dt];
       }
     }
+    if (tid == 0) next_unit = nxt;
   };
   if (RTW >= 2 && nown == 2) run(std::integral_constant<int, (RTW >= 2 ? 2 : 1)>{});
   else if (nown == 1) run(std::integral_constant<int, 1>{});
