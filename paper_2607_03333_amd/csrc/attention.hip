@@ -81,16 +81,16 @@ __device__ __forceinline__ float softmax_step(float (&sv)[8], float& m, float& l
 // --------------------------------------------------------------------------
 constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 bytes / 16
 // LDS stages per workgroup: 4 for two 4-wave workgroups on a compute unit, 8
-// for one 8-wave workgroup. A barrier publishes two stages (2 in flight
-// with 4 stages, 6 with 8). Against one stage per barrier (3 and 7 in
-// flight) this halves the barriers, and the waves drift apart inside a pair
-// instead of all reading the same operands right after every barrier:
-// K = 16 verify step 8-10% faster, K = 50 verify 2-3%, the decode batches
-// 1-2%, though fewer stages stay in flight. Four per barrier: slower.
+// for one 8-wave workgroup. A barrier publishes one stage (4-wave: 3 in
+// flight) or two (8-wave: 6 in flight). Two stages per barrier halve the
+// barriers of the many-row loop, and its waves drift apart inside a pair
+// instead of all reading the same operands right after every barrier (K = 16
+// verify step 8-10% faster, K = 50 verify 2-3%, probe prefill 1-2%; four per
+// barrier: slower). The 4-wave loop stays at one stage per barrier.
 template <int NW>
 constexpr int ring_of() { return NW == 4 ? 4 : 8; }
 template <int NW>
-constexpr int stages_per_barrier() { return 2; }
+constexpr int stages_per_barrier() { return NW == 4 ? 1 : 2; }
 
 // Wait until at most `after` (0..7) stages of this wave's direct-to-LDS
 // loads (LPW per stage), and no older vector load, are still in flight.
