@@ -47,16 +47,18 @@ __device__ __forceinline__ float softmax_step(float (&sv)[8], float& m, float& l
 }
 
 // --------------------------------------------------------------------------
-// bf16 partial attention. A persistent workgroup of 4 waves works through its
-// list of units; a unit is a token range of one work item and up to 4*RTW
-// 16-row tiles of its query rows; wave w computes tiles c, c+4 (c = w, or w + 2
-// mod 4 in the second workgroup of a compute unit). The range streams through a ring of kRing LDS slots, one
-// 32-token K/V tile ("stage", 16 KB) each, filled by direct global-to-LDS
-// 16-byte loads (global_load_lds_dwordx4: lane i of an instruction lands at
-// the instruction's LDS base + 16*i), so kRing-1 stages stay in flight without
-// holding registers. Each wave issues 4 such loads per stage (waves 0-1 the K
-// half, waves 2-3 the V half); one barrier per stage publishes a slot to all
-// waves and frees the slot read in the previous stage.
+// bf16 partial attention. A persistent workgroup of NW waves (4, two per
+// compute unit; or 8, one per compute unit) works through its list of units;
+// a unit is a token range of one work item and up to NW*RTW 16-row tiles of
+// its query rows; wave w computes tiles c, c + NW, ... (c = w, or w + 2 mod 4
+// in the second 4-wave workgroup of a compute unit). The range streams through
+// a ring of kRing LDS slots, one 32-token K/V tile ("stage", 16 KB) each,
+// filled by direct global-to-LDS 16-byte loads (global_load_lds_dwordx4: lane
+// i of an instruction lands at the instruction's LDS base + 16*i), so the
+// stages in flight hold no registers. Each wave issues 16/NW such loads per
+// stage (the first half of the waves the K half, the others the V half); a
+// barrier publishes the next stage (4 waves) or the next two (8 waves) to all
+// waves and frees the slots read before it.
 //
 // LDS slot layout (1024 chunks of 16 bytes). Bank model (measured on
 // gfx950): 64 banks of 4 bytes, so a 16-byte slot s sits in bank group
