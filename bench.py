@@ -26,6 +26,7 @@ plain streaming-read kernels measured in the same process.
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -47,10 +48,17 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_03333_amd", "csrc", f)
 
 
 def kernel_source_hash():
+    """First 16 hex digits of the sha256 of the attention kernel's code
+    (KERNEL_SOURCES with comments and whitespace removed): counters taken on
+    one code stay valid across comment edits and no longer match once the
+    code changes."""
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 
