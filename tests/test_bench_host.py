@@ -60,3 +60,23 @@ def test_mfma_ridge_points():
     # bf16: 2.5 PFLOP/s over 8 TB/s; fp32 MFMA: 157.3 TFLOP/s over 8 TB/s
     assert abs(b.MFMA_PEAK_TFLOPS["bf16"] * 1e12 / (b.HBM_PEAK_GBPS * 1e9) - 312.5) < 1e-9
     assert abs(b.MFMA_PEAK_TFLOPS["f32"] * 1e12 / (b.HBM_PEAK_GBPS * 1e9) - 19.6625) < 1e-9
+
+
+def test_kernel_hash_follows_the_code_not_its_comments(tmp_path):
+    # the counters in profiles/ stay matched across comment and layout edits
+    # of the kernel sources and stop matching once a line of code changes
+    b = _bench_module()
+    srcs = []
+    for i, path in enumerate(b.KERNEL_SOURCES):
+        with open(path) as f:
+            text = f.read()
+        p = tmp_path / f"src{i}"
+        p.write_text(text)
+        srcs.append((p, text))
+    b.KERNEL_SOURCES = [str(p) for p, _ in srcs]
+    h0 = b.kernel_source_hash()
+    p0, t0 = srcs[0]
+    p0.write_text("// a note\n" + t0.replace("\n", "\n  ", 3) + "\n/* another\n note */\n")
+    assert b.kernel_source_hash() == h0
+    p0.write_text(t0 + "\nconstexpr int kNotInTheKernel = 1;\n")
+    assert b.kernel_source_hash() != h0
