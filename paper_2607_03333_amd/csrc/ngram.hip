@@ -30,7 +30,8 @@ __global__ void __launch_bounds__(256) ngram_scan(NgramArgs a) {
   const int64_t L = a.seq_off[s + 1] - base;
   const int32_t* t = a.tokens + base;
   __shared__ int32_t tail[kNgramMaxN];
-  if (threadIdx.x < a.n_max && threadIdx.x < L) tail[threadIdx.x] = t[L - 1 - threadIdx.x];
+  const int tx = static_cast<int>(threadIdx.x);
+  if (tx < a.n_max && tx < L) tail[tx] = t[L - 1 - tx];
   __syncthreads();
   uint64_t best = 0;
   const int64_t lo = static_cast<int64_t>(c) * kNgramChunk;
