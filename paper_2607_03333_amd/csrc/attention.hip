@@ -88,7 +88,11 @@ constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 by
 // barriers of the many-row loop, and its waves drift apart inside a pair
 // instead of all reading the same operands right after every barrier (K = 16
 // verify step 8-10% faster, K = 50 verify 2-3%, probe prefill 1-2%; four per
-// barrier: slower). The 4-wave loop stays at one stage per barrier.
+// barrier: slower). The 4-wave loop stays at one stage per barrier. In the
+// 8-wave loop the second stage of a pair is published with the first, so its
+// K operands are read into registers behind the first stage's softmax and its
+// score products start without an LDS round trip (K = 16 verify step 3%
+// faster, K = 50 2%, probe prefill 1%).
 template <int NW>
 constexpr int ring_of() { return NW == 4 ? 4 : 8; }
 template <int NW>
@@ -163,6 +167,15 @@ __device__ __forceinline__ u32x2 tab_read(uint32_t addr) {
   return r;
 }
 __device__ __forceinline__ void tab_wait(u32x2& r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r) : : "memory"); }
+
+// Wait for all LDS reads but the 8 issued last (LDS reads complete in order).
+__device__ __forceinline__ void lds_wait_but8(u32x4 (&r)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(8)"
+               : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]),
+                 "+v"(r[7])
+               :
+               : "memory");
+}
 
 template <int N>
 __device__ __forceinline__ void lds_wait(u32x4 (&r)[N]) {
@@ -257,7 +270,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   // each next one at the end of the current unit, before its partial results
   // are stored, so neither the atomic's round trip nor the stores' sit
   // between two units. A barrier without a memory fence publishes the take.
-  if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
+  if (tid == 0) next_unit = atomicAdd(a.cursors + list * kCursorStride, 1);
   for (;;) {
   barrier_lds();
   const int taken = __builtin_amdgcn_readfirstlane(next_unit);
@@ -265,7 +278,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   const WaveDesc w = load_wave_desc(a.waves + list0 + taken);
   if (w.item < 0) {  // padding (not emitted on persistent lists): every wave reads next_unit first
     barrier_nofence();
-    if (tid == 0) next_unit = atomicAdd(a.cursors + list, 1);
+    if (tid == 0) next_unit = atomicAdd(a.cursors + list * kCursorStride, 1);
     continue;
   }
   const ItemDesc it = load_item_desc(a.items + w.item);
@@ -423,16 +436,22 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   // exact maximum.
   const float c = a.scale_log2;
   // One stage for NT owned tiles, reading ring slot (st % kRing).
-  auto compute_tiles = [&](auto nt_c, int st) __attribute__((always_inline)) {
-    constexpr int NT = decltype(nt_c)::value;
-    const int tb = tb0 + st * kTileTokens;
+  auto read_k = [&](u32x4 (&kr)[8], int st) __attribute__((always_inline)) {
     const uint32_t soff = static_cast<uint32_t>(st % kRing) * (kStageChunks * 16);
-    const bool edge = tb < w.tok_lo || tb + kTileTokens > tok_hi || tb + kTileTokens - 1 > hmin;
-    u32x4 kr[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) kr[i] = lds_read_b128(kaddr[i] + soff);
 #pragma unroll
     for (int i = 0; i < 4; ++i) kr[4 + i] = lds_read_b128<1024>(kaddr[i] + soff);
+  };
+  // PRE: kr already holds this stage's K (read during the previous stage).
+  // NEXT: read the next stage's K into kr behind this stage's softmax.
+  auto compute_tiles = [&](auto nt_c, auto pre_c, auto next_c, int st, u32x4 (&kr)[8]) __attribute__((always_inline)) {
+    constexpr int NT = decltype(nt_c)::value;
+    constexpr bool PRE = decltype(pre_c)::value, NEXT = decltype(next_c)::value;
+    const int tb = tb0 + st * kTileTokens;
+    const uint32_t soff = static_cast<uint32_t>(st % kRing) * (kStageChunks * 16);
+    const bool edge = tb < w.tok_lo || tb + kTileTokens > tok_hi || tb + kTileTokens - 1 > hmin;
+    if constexpr (!PRE) read_k(kr, st);
     lds_wait(kr);
     f32x4 sc[NT][2];
 #pragma unroll
@@ -552,7 +571,12 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
         for (int j = 0; j < NT; ++j) mask_tile(j);
       }
       bf16x8 pop = softmax_tile(0);
-      lds_wait(vr);
+      if constexpr (NEXT) {
+        read_k(kr, st + 1);
+        lds_wait_but8(vr);
+      } else {
+        lds_wait(vr);
+      }
       zero_past_range();
 #pragma unroll
       for (int j = 1; j < NT; ++j) {
@@ -611,27 +635,33 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     u32x2 ent[kPer];
 #pragma unroll
     for (int q = 0; q < kPer; ++q) ent[q] = stage_entries(kAhead + q);
-    for (int st = 0; st < nstage; ++st) {
-      if (st % kPer == 0) {
-        wait_stage<LPW>(max(0, min(kAhead - kPer, nstage - kPer - st)));
-        barrier_nofence();
+    u32x4 kr[8];
+    for (int st = 0; st < nstage; st += kPer) {
+      wait_stage<LPW>(max(0, min(kAhead - kPer, nstage - kPer - st)));
+      barrier_nofence();
 #pragma unroll
-        for (int q = 0; q < kPer; ++q) {
-          if (st + kAhead + q < nstage) {
-            tab_wait(ent[q]);
-            issue_stage(st + kAhead + q, ent[q]);
-          }
+      for (int q = 0; q < kPer; ++q) {
+        if (st + kAhead + q < nstage) {
+          tab_wait(ent[q]);
+          issue_stage(st + kAhead + q, ent[q]);
         }
-#pragma unroll
-        for (int q = 0; q < kPer; ++q) ent[q] = stage_entries(st + kRing + q);
       }
-      if constexpr (NT > 0) compute_tiles(nt_c, st);
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) ent[q] = stage_entries(st + kRing + q);
+      if constexpr (NT > 0) {
+        if constexpr (kPer == 2) {
+          compute_tiles(nt_c, std::false_type{}, std::true_type{}, st, kr);
+          if (st + 1 < nstage) compute_tiles(nt_c, std::true_type{}, std::false_type{}, st + 1, kr);
+        } else {
+          compute_tiles(nt_c, std::false_type{}, std::false_type{}, st, kr);
+        }
+      }
     }
     wait_vmcnt<0>();
     // Every wave has read this unit's take (the ring loop's barriers follow
     // it): take the next unit now.
     int nxt = 0;
-    if (tid == 0) nxt = atomicAdd(a.cursors + list, 1);
+    if (tid == 0) nxt = atomicAdd(a.cursors + list * kCursorStride, 1);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       float lt = l[j] + __shfl_xor(l[j], 16);
@@ -663,7 +693,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   if (a.tail_units > 0) {
     __syncthreads();  // every wave has read the last list take
     for (;;) {
-      if (tid == 0) next_unit = atomicAdd(a.cursors + a.n_lists, 1);
+      if (tid == 0) next_unit = atomicAdd(a.cursors + a.n_lists * kCursorStride, 1);
       __syncthreads();
       const int u = __builtin_amdgcn_readfirstlane(next_unit);
       if (u < 0 || u >= a.tail_units) break;
@@ -894,7 +924,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   // The attention launch is done with its cursors: return them to zero for
   // the workspace's next call.
   if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < a.n_cursors; i += 256) a.cursors[i] = 0;
+    for (int i = threadIdx.x; i < a.n_cursors; i += 256) a.cursors[i * kCursorStride] = 0;
   const int merge_blocks = (a.n_out + 3) / 4;
   if (static_cast<int>(blockIdx.x) >= merge_blocks) {
     // fused accept: one verify thread per wave

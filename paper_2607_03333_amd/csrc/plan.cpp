@@ -235,18 +235,44 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     // c + n_wg/2 when two share a compute unit), which take the list's units
     // in order through an atomic cursor: the faster workgroup of the pair
     // (the one dispatched first wins the instruction arbiter by age) simply
-    // takes more units, and compute units differ little in throughput, so a
-    // static balance between the lists suffices. A range with two row slices
+    // takes more units. The compute units of one accelerator die stream at
+    // about the same rate; the dies differ by a few percent (up to 13% on a
+    // small decode batch), which a static plan cannot know, but a shared list
+    // that every workgroup takes its last units from, to even that out at run
+    // time, cost more than it recovered (its one cursor serialises the
+    // takes), so the lists are balanced statically. A range with two row slices
     // puts both slices next to each other on one list, so the pair streams
     // its KV through one L2 at the same time.
     //
-    // Lists are balanced by water-filling on token cost, each unit also
-    // costing kUnitOverheadTokens for its start-up: ranges shorter than half
-    // a list's share go whole, longest first, to the least-loaded list;
-    // longer ranges are cut so that each piece tops the least-loaded list up
-    // to the share, a piece being at most one workgroup's share so that both
-    // workgroups of a list find work. Each list runs longest unit first, so
-    // its last units are short.
+    // Lists are balanced by water-filling on cost, each unit also costing
+    // kUnitOverheadTokens for its start-up: ranges shorter than half a list's
+    // share go whole, longest first, to the least-loaded list; longer ranges
+    // are cut so that each piece tops the least-loaded list up to the share,
+    // a piece being at most one workgroup's share so that both workgroups of
+    // a list find work. Each list runs longest unit first, so its last units
+    // are short.
+    //
+    // Cost of a token: one per row slice in 4-wave plans, whose stages are
+    // bound by HBM. The stages of 8-wave plans are bound by the matrix cores
+    // of the SIMD that holds the most row tiles (tile t is on SIMD t % 4), and
+    // one with 1, 2 or 3 tiles there costs 0.56, 0.71 or 0.80 of one with 4
+    // (measured: 1,236, 1,560, 1,773 and 2,211 cycles per 32-token stage), so
+    // a token of a slice costs kStageWeight[that count] / 1024 there.
+    const int64_t wunit = shape.waves == 8 ? 1024 : 1;  // cost of a token of a full slice
+    const int64_t ovh = kUnitOverheadTokens * wunit;    // start-up cost of a unit
+    std::vector<int64_t> tok_cost(items.size());        // cost of a token of the item, all slices
+    for (size_t it = 0; it < items.size(); ++it) {
+      if (wunit == 1) {
+        tok_cost[it] = slices_of[it];
+        continue;
+      }
+      static constexpr int64_t kStageWeight[5] = {0, 572, 722, 821, 1024};
+      tok_cost[it] = 0;
+      for (int32_t sl = 0; sl < slices_of[it]; ++sl) {
+        const int32_t tiles = (std::min(slice_rows, items[it].n_rows - sl * slice_rows) + 15) / 16;
+        tok_cost[it] += kStageWeight[std::min(4, (tiles + 3) / 4)];
+      }
+    }
     const int64_t per_list = per_cu == 2 ? 2 : 1;
     const int64_t lanes = n_wg / per_list;
     std::vector<std::vector<WaveDesc>> lists(lanes);
@@ -257,30 +283,29 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     auto place = [&](int32_t item, int32_t lo, int32_t hi, int32_t slices) {
       const int64_t c = least();
       for (int32_t s = 0; s < slices; ++s) lists[c].push_back(desc(item, lo, hi, s));
-      load[c] += (static_cast<int64_t>(hi - lo) + kUnitOverheadTokens) * slices;
+      load[c] += static_cast<int64_t>(hi - lo) * tok_cost[item] + ovh * slices;
     };
     std::vector<size_t> order(items.size());
     for (size_t i = 0; i < order.size(); ++i) order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](size_t x, size_t y) {
       return item_range[x]->hi - item_range[x]->lo > item_range[y]->hi - item_range[y]->lo;
     });
-    // The share of a list: the fixed point of share = (tokens +
-    // kUnitOverheadTokens * units) / lanes, where a range shorter than half
-    // the share is one unit per slice and a longer one is cut into pieces of
-    // share / max(slices, workgroups per list) - kUnitOverheadTokens.
+    // The share of a list: the fixed point of share = (cost of the tokens +
+    // start-up cost of the units) / lanes, where a range cheaper than half
+    // the share is one unit per slice and a longer one is cut into pieces
+    // whose units cost share / max(slices, workgroups per list) each.
     int64_t tokens = 0;
     for (size_t it = 0; it < items.size(); ++it)
-      tokens += static_cast<int64_t>(item_range[it]->hi - item_range[it]->lo) * slices_of[it];
+      tokens += static_cast<int64_t>(item_range[it]->hi - item_range[it]->lo) * tok_cost[it];
     auto unit_cost_share = [&](int64_t share) {
       int64_t units = 0;
       for (size_t it = 0; it < items.size(); ++it) {
-        const int64_t len = item_range[it]->hi - item_range[it]->lo;
-        const int64_t piece =
-            std::max<int64_t>(kTileTokens, share / std::max<int64_t>(slices_of[it], per_list) - kUnitOverheadTokens);
-        units += ((len + kUnitOverheadTokens) * slices_of[it] <= share / 2 ? 1 : (len + piece - 1) / piece) *
-                 slices_of[it];
+        const int64_t len = item_range[it]->hi - item_range[it]->lo, sl = slices_of[it];
+        const int64_t piece = std::max<int64_t>(
+            kTileTokens, (share / std::max<int64_t>(sl, per_list) - ovh) * sl / tok_cost[it]);
+        units += (len * tok_cost[it] + ovh * sl <= share / 2 ? 1 : (len + piece - 1) / piece) * sl;
       }
-      return (tokens + kUnitOverheadTokens * units + lanes - 1) / lanes;
+      return (tokens + ovh * units + lanes - 1) / lanes;
     };
     int64_t share = (tokens + lanes - 1) / lanes;
     for (int iter = 0; iter < 32; ++iter) {
@@ -293,7 +318,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     // its own start-up cost; the level is then raised by that overflow spread
     // over all lists and the fill repeated, keeping the lowest maximum.
     const int64_t min_piece =  // an eighth of a workgroup's share, 64..512 tokens
-        std::min<int64_t>(kMinPieceTokens, std::max<int64_t>(64, share / per_list / 8 / kTileTokens * kTileTokens));
+        std::min<int64_t>(kMinPieceTokens,
+                          std::max<int64_t>(64, share / wunit / per_list / 8 / kTileTokens * kTileTokens));
     auto fill = [&](int64_t level, int64_t* overflow) {
       for (auto& l : lists) l.clear();
       std::fill(load.begin(), load.end(), 0);
@@ -302,14 +328,15 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
         for (size_t it : order) {
           const Range& rg = *item_range[it];
           const int32_t slices = slices_of[it];
-          const bool small = (static_cast<int64_t>(rg.hi - rg.lo) + kUnitOverheadTokens) * slices <= share / 2;
+          const bool small = static_cast<int64_t>(rg.hi - rg.lo) * tok_cost[it] + ovh * slices <= share / 2;
           if (small != (pass == 0)) continue;
           for (int32_t lo = rg.lo; lo < rg.hi;) {
             int64_t want = kMaxUnitTokens;
             // a piece tops the list up, but is at most one workgroup's share
-            if (!small) want = std::min(level - load[least()], level / per_list * slices) / slices - kUnitOverheadTokens;
+            if (!small)
+              want = (std::min(level - load[least()], level / per_list * slices) - ovh * slices) / tok_cost[it];
             const int32_t hi = cut_piece(lo, rg.hi, want, min_piece);
-            if (!small && want < min_piece) *overflow += (hi - lo + kUnitOverheadTokens) * slices;
+            if (!small && want < min_piece) *overflow += static_cast<int64_t>(hi - lo) * tok_cost[it] + ovh * slices;
             place(static_cast<int32_t>(it), lo, hi, slices);
             lo = hi;
           }
@@ -327,7 +354,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
         best = lists;
       }
       if (overflow == 0) break;
-      level += std::max<int64_t>(kTileTokens, (overflow + lanes - 1) / lanes);
+      level += std::max<int64_t>(kTileTokens * wunit, (overflow + lanes - 1) / lanes);
     }
     lists.swap(best);
     wg_off.push_back(0);
@@ -459,7 +486,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   // partial outputs and their (m, l) pairs.
   p.off_ws_cursors = 0;
   p.n_cursors = shape.persistent ? p.n_lists + 1 : 0;
-  p.control_bytes = align256(static_cast<size_t>(p.n_cursors) * sizeof(int32_t));
+  p.control_bytes = static_cast<size_t>(p.n_cursors) * kCursorStride * sizeof(int32_t);
   p.off_ws_o = p.control_bytes;
   p.off_ws_ml = p.off_ws_o + align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
   p.workspace_bytes = p.off_ws_ml + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
