@@ -5,6 +5,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <queue>
 
 namespace spork {
 namespace {
@@ -277,13 +278,15 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     const int64_t lanes = n_wg / per_list;
     std::vector<std::vector<WaveDesc>> lists(lanes);
     std::vector<int64_t> load(lanes, 0);
-    auto least = [&]() {
-      return static_cast<int64_t>(std::min_element(load.begin(), load.end()) - load.begin());
-    };
+    // The least-loaded list (the lowest index among equals), kept in a heap.
+    std::priority_queue<std::pair<int64_t, int64_t>, std::vector<std::pair<int64_t, int64_t>>, std::greater<>> heap;
+    auto least = [&]() { return heap.top().second; };
     auto place = [&](int32_t item, int32_t lo, int32_t hi, int32_t slices) {
       const int64_t c = least();
+      heap.pop();
       for (int32_t s = 0; s < slices; ++s) lists[c].push_back(desc(item, lo, hi, s));
       load[c] += static_cast<int64_t>(hi - lo) * tok_cost[item] + ovh * slices;
+      heap.push({load[c], c});
     };
     std::vector<size_t> order(items.size());
     for (size_t i = 0; i < order.size(); ++i) order[i] = i;
@@ -323,6 +326,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     auto fill = [&](int64_t level, int64_t* overflow) {
       for (auto& l : lists) l.clear();
       std::fill(load.begin(), load.end(), 0);
+      heap = {};
+      for (int64_t c = 0; c < lanes; ++c) heap.push({0, c});
       *overflow = 0;
       for (int pass = 0; pass < 2; ++pass) {
         for (size_t it : order) {
