@@ -649,3 +649,35 @@ def test_plan_advance_refuses_what_it_cannot_absorb():
     assert e.value.code == spork.SPORK_E_CAPACITY and "reserve" in str(e.value)
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)
+
+
+def test_eight_wave_plan_weights_tokens_by_row_tiles():
+    """8-wave plans cost a token of a row slice by the row tiles its busiest
+    SIMD holds (tile t on SIMD t % 4; 1-4 tiles weigh 572, 722, 821 and 1024
+    in 1/1024, from measured stage times) plus 128 tokens of start-up per
+    unit: on the full-size probe prefill, whose slices hold 1-16 tiles, the
+    compute units' lists are balanced under that cost (they are not under a
+    plain token count), and its control words hold one 256-byte line per
+    cursor (one per list plus the argmax cursor)."""
+    wl = _full_size("prefill")
+    c, p = _plan_for(wl)
+    info, img = _decode_image(p)
+    assert info["attn_waves"] == 8
+    n_lists = info["attn_grid"]
+    raw = img.view(np.int32)
+    nu = info["n_units"]
+    units = raw[: nu * 6].reshape(nu, 6)
+    al = -(-(n_lists + 1) * 4 // 256) * 256 // 4
+    wg_off = raw[info["image_bytes"] // 4 - al:][: n_lists + 1]
+    weight = {1: 572, 2: 722, 3: 821, 4: 1024}
+    cost, tokens = np.zeros(n_lists), np.zeros(n_lists)
+    for x in range(n_lists):
+        for u in units[wg_off[x]:wg_off[x + 1]]:
+            tiles = (int(u[4]) + 15) // 16
+            cost[x] += int(u[2] - u[1]) * weight[min(4, (tiles + 3) // 4)] + 128 * 1024
+            tokens[x] += int(u[2] - u[1]) + 128
+    assert cost.max() <= cost.mean() * 1.02, cost.max() / cost.mean()
+    assert tokens.max() > tokens.mean() * 1.05  # a token count alone would not balance these lists
+    assert info["control_bytes"] == (n_lists + 1) * 256
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
