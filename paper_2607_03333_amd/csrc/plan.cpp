@@ -20,6 +20,12 @@ struct Range {
   std::vector<int32_t> threads;
 };
 
+// Relative cost of a 32-token stage of the 8-wave kernel by the row tiles
+// its busiest SIMD holds (tile t is on SIMD t % 4), in 1/1024 of a full one:
+// measured 1,236, 1,560, 1,773 and 2,211 cycles for 1 to 4 tiles.
+constexpr int64_t kStageWeight8[5] = {0, 572, 722, 821, 1024};
+int64_t stage_weight8(int32_t slice_tiles) { return kStageWeight8[std::min(4, (slice_tiles + 3) / 4)]; }
+
 struct Unit {  // one token segment of one item, split over `slices` row slices
   int32_t item, lo, hi, slices;
   int64_t cost() const { return static_cast<int64_t>(hi - lo) * slices; }
@@ -163,6 +169,26 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     const int32_t slices = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
     row_tiles = std::max(row_tiles, (tiles + slices - 1) / slices);
   }
+  // 8-wave plans: the slice size (one for the whole plan) that streams the
+  // ranges at the least stage cost, fuller slices first among equals. Near-
+  // equal slices can leave every slice with four tiles on its busiest SIMD
+  // (26 tiles as 13 + 13 cost two full stages per 32 tokens; as 16 + 10,
+  // one full and one three-tile stage).
+  if (shape.persistent && shape.waves == 8) {
+    int64_t best = INT64_MAX;
+    for (int32_t rt = shape.unit_tiles_max; rt >= 1; --rt) {
+      int64_t cost = 0;
+      for (size_t r = 0; r < ranges.size(); ++r) {
+        const int64_t len = ranges[r].hi - ranges[r].lo;
+        for (int32_t done = 0; done < range_rows[r]; done += rt * 16)
+          cost += len * stage_weight8((std::min(rt * 16, range_rows[r] - done) + 15) / 16);
+      }
+      if (cost < best) {
+        best = cost;
+        row_tiles = rt;
+      }
+    }
+  }
   const int32_t slice_rows = row_tiles * 16;
   p.row_tiles = row_tiles;
 
@@ -255,10 +281,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     //
     // Cost of a token: one per row slice in 4-wave plans, whose stages are
     // bound by HBM. The stages of 8-wave plans are bound by the matrix cores
-    // of the SIMD that holds the most row tiles (tile t is on SIMD t % 4), and
-    // one with 1, 2 or 3 tiles there costs 0.56, 0.71 or 0.80 of one with 4
-    // (measured: 1,236, 1,560, 1,773 and 2,211 cycles per 32-token stage), so
-    // a token of a slice costs kStageWeight[that count] / 1024 there.
+    // of the SIMD that holds the most row tiles, so a token of a slice costs
+    // stage_weight8(its tiles) / 1024 there.
     const int64_t wunit = shape.waves == 8 ? 1024 : 1;  // cost of a token of a full slice
     const int64_t ovh = kUnitOverheadTokens * wunit;    // start-up cost of a unit
     std::vector<int64_t> tok_cost(items.size());        // cost of a token of the item, all slices
@@ -267,12 +291,9 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
         tok_cost[it] = slices_of[it];
         continue;
       }
-      static constexpr int64_t kStageWeight[5] = {0, 572, 722, 821, 1024};
       tok_cost[it] = 0;
-      for (int32_t sl = 0; sl < slices_of[it]; ++sl) {
-        const int32_t tiles = (std::min(slice_rows, items[it].n_rows - sl * slice_rows) + 15) / 16;
-        tok_cost[it] += kStageWeight[std::min(4, (tiles + 3) / 4)];
-      }
+      for (int32_t sl = 0; sl < slices_of[it]; ++sl)
+        tok_cost[it] += stage_weight8((std::min(slice_rows, items[it].n_rows - sl * slice_rows) + 15) / 16);
     }
     const int64_t per_list = per_cu == 2 ? 2 : 1;
     const int64_t lanes = n_wg / per_list;
