@@ -681,3 +681,22 @@ def test_eight_wave_plan_weights_tokens_by_row_tiles():
     assert info["control_bytes"] == (n_lists + 1) * 256
     spork.spork_plan_destroy(p)
     spork.spork_cache_destroy(c)
+
+
+def test_eight_wave_slices_by_stage_cost():
+    """The K = 50 verify step's 408 rows per KV head (26 tiles) go as slices
+    of 16 and 10 tiles (16 + 10: a full stage and a three-tile one per 32
+    tokens), not as two near-equal 13-tile slices (four tiles on the busiest
+    SIMD of each); the 136 rows of the K = 16 step stay one 9-tile slice."""
+    for case, rows, want in (("verify-k50", 408, {256, 152}), ("3", 136, {136})):
+        wl = _full_size(case)
+        c, p = _plan_for(wl)
+        info, img = _decode_image(p)
+        assert info["attn_waves"] == 8
+        nu = info["n_units"]
+        units = img.view(np.int32)[: nu * 6].reshape(nu, 6)
+        assert set(int(x) for x in units[:, 4]) == want
+        # every unit's slice starts on a slice boundary of the item's rows
+        assert set(int(x) for x in units[:, 3]) == ({0, 256} if case == "verify-k50" else {0})
+        spork.spork_plan_destroy(p)
+        spork.spork_cache_destroy(c)
