@@ -167,6 +167,11 @@ __device__ __forceinline__ u32x2 tab_read(uint32_t addr) {
   return r;
 }
 __device__ __forceinline__ void tab_wait(u32x2& r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r) : : "memory"); }
+template <int N>
+__device__ __forceinline__ void tab_wait_all(u32x2 (&r)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) tab_wait(r[i]);
+}
 
 // Wait for all LDS reads but the 8 issued last (LDS reads complete in order).
 __device__ __forceinline__ void lds_wait_but8(u32x4 (&r)[8]) {
@@ -658,6 +663,13 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
       }
     }
     wait_vmcnt<0>();
+    // The LDS reads issued by inline assembly are invisible to the compiler's
+    // wait tracking: a K prefetch for a stage past the unit's end and the
+    // table entries read one barrier ahead are still in flight here. Wait
+    // for them with their registers as operands, so that no later value is
+    // placed in those registers before the reads have written them.
+    tab_wait_all(ent);
+    if constexpr (kPer == 2) lds_wait(kr);
     // Every wave has read this unit's take (the ring loop's barriers follow
     // it): take the next unit now.
     int nxt = 0;
