@@ -150,20 +150,17 @@ __device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
 }
 
 // The block-table entries of one stage, read from LDS at a wave-uniform
-// address without a wait: two adjacent entries (16-token blocks, one per half
-// of the stage) or one (32-token blocks). tab_wait() waits for the read and
-// takes the registers as in-out operands, so no use moves above it.
+// address without a wait: the two entries of the stage's halves (the staged
+// table holds each 32-token block's entry twice, so both block sizes read one
+// pair). tab_wait() waits for the read and takes the registers as in-out
+// operands, so no use moves above it. The read's own output registers are the
+// pair: any copy of a register the read has not yet written (say, building
+// the pair from one 32-bit result) would copy stale contents, since the
+// compiler does not know the read is still in flight.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-template <int BS>
 __device__ __forceinline__ u32x2 tab_read(uint32_t addr) {
   u32x2 r;
-  if constexpr (BS == 16) {
-    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr) : "memory");
-  } else {
-    uint32_t x;
-    asm volatile("ds_read_b32 %0, %1" : "=v"(x) : "v"(addr) : "memory");
-    r = u32x2{x, x};
-  }
+  asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr) : "memory");
   return r;
 }
 __device__ __forceinline__ void tab_wait(u32x2& r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r) : : "memory"); }
@@ -325,16 +322,20 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     rdesc[j] = a.rows[it.row_off + w.row0 + (has_row[j] ? i : 0)];  // padding lanes: the unit's first row, unused
   }
   // The unit's slice of the block table, staged in LDS before the ring
-  // starts (tab[i] = table entry tb0/BS + i, clamped to the table; stage st
-  // uses entries 2*st and 2*st + 1 with 16-token blocks, st with 32-token
-  // ones) and read per stage outside the compiler's view (a vector load of
+  // starts and read per stage outside the compiler's view (a vector load of
   // the table inside the loop would make its wait also wait for every
-  // direct-to-LDS load issued before it), one stage ahead of its use.
+  // direct-to-LDS load issued before it), one stage ahead of its use. Stage
+  // st reads the pair at tab[2*st]: with 16-token blocks tab[i] = table entry
+  // tb0/BS + i, with 32-token blocks tab[2i] = tab[2i + 1] = entry tb0/BS + i
+  // (entries clamped to the table).
+  constexpr int kDup = BS == 16 ? 1 : 2;
   const int tab0 = tb0 / BS;
-  const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks);  // planner keeps it below
+  const int ntab = min((tb0 + nstage * kTileTokens + 16) / BS - tab0 + 1, kUnitBlocks / kDup);  // planner keeps it below
   for (int i = tid; i < ntab; i += NT_) {
     const int bi = tab0 + i;
-    tab[i] = table[bi < nb ? bi : nb - 1];
+    const int e = table[bi < nb ? bi : nb - 1];
+#pragma unroll
+    for (int d = 0; d < kDup; ++d) tab[kDup * i + d] = e;
   }
 
   // Query operands and row horizons of this wave's tiles. A padding lane
@@ -396,7 +397,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
   const uint32_t tab_base = lds_addr(&tab[0]);
   auto stage_entries = [&](int st) __attribute__((always_inline)) {
     const int s = min(st, nstage - 1);
-    return tab_read<BS>(tab_base + 4u * static_cast<uint32_t>(BS == 16 ? 2 * s : s));
+    return tab_read(tab_base + 8u * static_cast<uint32_t>(s));
   };
   // Issue the direct-to-LDS loads of stage `st` into ring slot st % kRing,
   // `ent` holding its table entries (already waited for).

@@ -448,7 +448,9 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   for (size_t u = 0; u < waves.size(); ++u) {
     WaveDesc& w = waves[u];
     if (w.item < 0) continue;
-    if (unit_table_span(w.tok_lo, w.tok_hi, shape.block_size) > kUnitTableEntries) return "internal: unit too long";
+    // the bf16 kernel stages a 32-token block's entry twice
+    if (unit_table_span(w.tok_lo, w.tok_hi, shape.block_size) * (shape.block_size == 32 ? 2 : 1) > kUnitTableEntries)
+      return "internal: unit too long";
     w.partial = partial;
     partial += w.nrows;
     // the last unit of a private range is the one later decode steps extend

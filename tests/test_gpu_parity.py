@@ -154,10 +154,7 @@ def test_verify_k50():
 @pytest.mark.parametrize("index,shrink", [
     (0, dict(block_size=32)),                                                           # fp32 decode + verify
     (4, dict(sessions=3, prefix=1000, suffix=("loguniform", 1, 400), vocab=3000, block_size=32)),
-    pytest.param(2, dict(sessions=2, prefix=777, suffix=("uniform", 1, 200), block_size=32),  # fork inside a block
-                 marks=pytest.mark.skip(reason="faulted the GPU once under a 4-wave loop variant (two stages per "
-                                               "barrier) that has been taken out; its cause is not shown, so the "
-                                               "case stays off the GPU")),
+    (2, dict(sessions=2, prefix=777, suffix=("uniform", 1, 200), block_size=32)),  # fork inside a block
 ])
 def test_block_size_32(index, shrink):
     wl = synth.make(index, **shrink)
