@@ -83,20 +83,20 @@ __device__ __forceinline__ float softmax_step(float (&sv)[8], float& m, float& l
 // --------------------------------------------------------------------------
 constexpr int kStageChunks = 1024;  // 32 tokens x (K + V) x 128 channels x 2 bytes / 16
 // LDS stages per workgroup: 4 for two 4-wave workgroups on a compute unit, 8
-// for one 8-wave workgroup. A barrier publishes one stage (4-wave: 3 in
-// flight) or two (8-wave: 6 in flight). Two stages per barrier halve the
-// barriers of the many-row loop, and its waves drift apart inside a pair
-// instead of all reading the same operands right after every barrier (K = 16
-// verify step 8-10% faster, K = 50 verify 2-3%, probe prefill 1-2%; four per
-// barrier: slower). The 4-wave loop stays at one stage per barrier. In the
-// 8-wave loop the second stage of a pair is published with the first, so its
-// K operands are read into registers behind the first stage's softmax and its
-// score products start without an LDS round trip (K = 16 verify step 3%
-// faster, K = 50 2%, probe prefill 1%).
+// for one 8-wave workgroup. A barrier publishes two stages (4-wave: 2 in
+// flight, 8-wave: 6). Against one stage per barrier this halves the barriers,
+// and the waves drift apart inside a pair instead of all reading the same
+// operands right after every barrier: K = 16 verify step 8-10% faster, K = 50
+// verify 2-3%, probe prefill 1-2%, and on the 4-wave decode loop (with a
+// stage fewer in flight) the Qwen3-4B batch 3.6% and the bench workload 1.6%
+// (the fork tree 0.8% slower); four per barrier: slower. In the 8-wave loop
+// the second stage of a pair is published with the first, so its K operands
+// are read into registers behind the first stage's softmax and its score
+// products start without an LDS round trip (K = 16 verify step 3% faster,
+// K = 50 2%, probe prefill 1%).
 template <int NW>
 constexpr int ring_of() { return NW == 4 ? 4 : 8; }
-template <int NW>
-constexpr int stages_per_barrier() { return NW == 4 ? 1 : 2; }
+constexpr int kPer = 2;  // stages a barrier publishes
 
 // Wait until at most `after` (0..7) stages of this wave's direct-to-LDS
 // loads (LPW per stage), and no older vector load, are still in flight.
@@ -610,12 +610,10 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     }
   };
 
-  // Prologue: the first kAhead stages in flight (kRing - 1 with one stage per
-  // barrier, kRing - 2 with two). The query rows, loaded before them,
-  // complete first (vector loads complete in order): this wait leaves only
-  // the prologue's loads in flight, and no wait for the query rows lands
-  // inside the loop.
-  constexpr int kPer = stages_per_barrier<NW>();
+  // Prologue: the first kAhead = kRing - 2 stages in flight. The query rows,
+  // loaded before them, complete first (vector loads complete in order):
+  // this wait leaves only the prologue's loads in flight, and no wait for the
+  // query rows lands inside the loop.
   constexpr int kAhead = kRing - kPer;
 #pragma unroll
   for (int st = 0; st < kAhead; ++st) {
@@ -655,11 +653,12 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
 #pragma unroll
       for (int q = 0; q < kPer; ++q) ent[q] = stage_entries(st + kRing + q);
       if constexpr (NT > 0) {
-        if constexpr (kPer == 2) {
+        if constexpr (NW == 8) {
           compute_tiles(nt_c, std::false_type{}, std::true_type{}, st, kr);
           if (st + 1 < nstage) compute_tiles(nt_c, std::true_type{}, std::false_type{}, st + 1, kr);
-        } else {
+        } else {  // the 4-wave compute reads each stage's K itself
           compute_tiles(nt_c, std::false_type{}, std::false_type{}, st, kr);
+          if (st + 1 < nstage) compute_tiles(nt_c, std::false_type{}, std::false_type{}, st + 1, kr);
         }
       }
     }
@@ -670,7 +669,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
     // for them with their registers as operands, so that no later value is
     // placed in those registers before the reads have written them.
     tab_wait_all(ent);
-    if constexpr (kPer == 2) lds_wait(kr);
+    if constexpr (NW == 8) lds_wait(kr);
     // Every wave has read this unit's take (the ring loop's barriers follow
     // it): take the next unit now.
     int nxt = 0;
