@@ -685,9 +685,17 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 ? 2 : 1)) attn_bf16(AttnArgs
           a.part_ml[2 * pr] = m[j];
           a.part_ml[2 * pr + 1] = lt;
         }
+        // bf16, in register order: the lane's 32 channels 16*dt + 4*g + i
+        // (dt = 0..7, i = 0..3) at row positions 32*g + 4*dt + i, four
+        // 16-byte stores.
+        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<__bf16*>(a.part_o) + pr * D + 32 * g);
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-          *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[j][dt];
+        for (int q = 0; q < 4; ++q) {
+          bf16x8 h;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] = static_cast<__bf16>(o[j][2 * q + (e >> 2)][e & 3]);
+          dst[q] = __builtin_bit_cast(u32x4, h);
+        }
       }
     }
     if (tid == 0) next_unit = nxt;
@@ -872,7 +880,7 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<f32x4*>(a.part_o + pr * D + 16 * dt + 4 * g) = o[t][dt];
+          *reinterpret_cast<f32x4*>(static_cast<float*>(a.part_o) + pr * D + 16 * dt + 4 * g) = o[t][dt];
       }
     }
   }
@@ -890,9 +898,40 @@ __global__ void __launch_bounds__(64) attn_f32(AttnArgs a) {
 // 0-7; unused slots repeat a valid row with weight 0. Batches after the
 // first rescale the running sums to the new maximum.
 // --------------------------------------------------------------------------
+// Partial rows are in the input dtype: fp32 rows in channel order, bf16 rows
+// (D = 128) in the bf16 attention writer's register order, channel
+// 16*dt + 4*g + i at position 32*g + 4*dt + i. Lane `lane` reads positions
+// PER*lane .. PER*lane + PER - 1 of every partial row (one coalesced pass
+// over the row) and merges the channels stored there: channel PER*lane + e
+// (fp32), or, for bf16, the pair merge_channel() + e (g = lane / 16,
+// dt = lane / 2 mod 8, i = 2 * (lane mod 2) and i + 1).
+template <int D, typename PT>
+__device__ __forceinline__ int merge_channel(int lane) {
+  if constexpr (std::is_same<PT, float>::value) {
+    return lane * (D / 64);
+  } else {
+    static_assert(D == 128, "bf16 partial rows are 128 channels");
+    return 16 * ((lane >> 1) & 7) + 4 * (lane >> 4) + 2 * (lane & 1);
+  }
+}
+
+template <int D, typename PT>
+__device__ __forceinline__ void load_partial(const AttnArgs& a, size_t row, int lane, float (&po)[D / 64]) {
+  constexpr int PER = D / 64;
+  if constexpr (std::is_same<PT, float>::value) {
+    const float* src = static_cast<const float*>(a.part_o) + row * D + lane * PER;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) po[e] = src[e];
+  } else {
+    const uint32_t w = reinterpret_cast<const uint32_t*>(static_cast<const __bf16*>(a.part_o) + row * D)[lane];
+    po[0] = __uint_as_float(w << 16);
+    po[1] = __uint_as_float(w & 0xFFFF0000u);
+  }
+}
+
 // One batch of at most B partials (entries c0 .. c0 + k - 1 of the output's
 // list), folded into the running (max, sum, accumulator).
-template <int B, int D>
+template <int B, int D, typename PT>
 __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bool first, int lane, float& run_max,
                                             float& mu, float& sum, float (&acc)[D / 64]) {
   constexpr int PER = D / 64;
@@ -900,12 +939,7 @@ __device__ __forceinline__ void merge_batch(const AttnArgs& a, int c0, int k, bo
   const float2 ml = reinterpret_cast<const float2*>(a.part_ml)[c0 + min(lane, k - 1)];
   float po[B][PER];
 #pragma unroll
-  for (int i = 0; i < B; ++i) {
-    const int idi = c0 + min(i, k - 1);
-    const float* src = a.part_o + static_cast<size_t>(idi) * D + lane * PER;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) po[i][e] = src[e];
-  }
+  for (int i = 0; i < B; ++i) load_partial<D, PT>(a, static_cast<size_t>(c0 + min(i, k - 1)), lane, po[i]);
   const bool live = lane < k;
   const float pm = live ? ml.x : kNegInf;
   const float pl = live ? ml.y : 0.0f;
@@ -953,12 +987,13 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
   float mu = 0.0f, sum = 0.0f, run_max = kNegInf;
   if (end - beg <= 4) {
-    merge_batch<4, D>(a, beg, end - beg, true, lane, run_max, mu, sum, acc);
+    merge_batch<4, D, OutT>(a, beg, end - beg, true, lane, run_max, mu, sum, acc);
   } else {
-    for (int c0 = beg; c0 < end; c0 += 8) merge_batch<8, D>(a, c0, min(8, end - c0), c0 == beg, lane, run_max, mu, sum, acc);
+    for (int c0 = beg; c0 < end; c0 += 8)
+      merge_batch<8, D, OutT>(a, c0, min(8, end - c0), c0 == beg, lane, run_max, mu, sum, acc);
   }
   const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
-  OutT* out = static_cast<OutT*>(a.out) + static_cast<size_t>(o) * D + lane * PER;
+  OutT* out = static_cast<OutT*>(a.out) + static_cast<size_t>(o) * D + merge_channel<D, OutT>(lane);
 #pragma unroll
   for (int e = 0; e < PER; ++e) out[e] = static_cast<OutT>(acc[e] * inv);
   if (lane == 0 && a.lse != nullptr)

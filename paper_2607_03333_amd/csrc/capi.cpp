@@ -506,7 +506,7 @@ static int attention(const spork_plan* plan, const void* dev_image, const void* 
   a.out = out;
   a.lse = lse;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  a.part_o = reinterpret_cast<float*>(ws + p.off_ws_o);
+  a.part_o = ws + p.off_ws_o;
   a.part_ml = reinterpret_cast<float*>(ws + p.off_ws_ml);
   a.n_cursors = p.n_cursors;
   // The persistent bf16 kernel takes its units through cursors that are zero

@@ -46,7 +46,10 @@ struct AttnArgs {
   const void* v_cache;
   void* out;
   float* lse;
-  float* part_o;   // [n_partials][head_dim] unnormalised partial outputs
+  // [n_partials][head_dim] unnormalised partial outputs in the input dtype;
+  // bf16 rows hold their channels in the bf16 writer's register order (see
+  // the merge in attention.hip), fp32 rows in channel order.
+  void* part_o;
   float* part_ml;  // [n_partials][2] running max (base 2) and sum
   // Verify step: accept units appended to the merge grid (acc.n_verify of them).
   AcceptArgs acc;

@@ -516,7 +516,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   p.n_cursors = shape.persistent ? p.n_lists + 1 : 0;
   p.control_bytes = static_cast<size_t>(p.n_cursors) * kCursorStride * sizeof(int32_t);
   p.off_ws_o = p.control_bytes;
-  p.off_ws_ml = p.off_ws_o + align256(static_cast<size_t>(partial) * shape.head_dim * sizeof(float));
+  p.off_ws_ml = p.off_ws_o + align256(static_cast<size_t>(partial) * shape.head_dim * shape.elem_bytes);
   p.workspace_bytes = p.off_ws_ml + align256(static_cast<size_t>(partial) * 2 * sizeof(float));
   *out = std::move(p);
   return "";

@@ -40,7 +40,8 @@ struct Plan {
   size_t off_waves = 0, off_items = 0, off_rows = 0, off_tables = 0, off_merge_off = 0,
          off_part_slot = 0, off_wg_off = 0;
   // Workspace: control words first (zero between calls: the list cursors of
-  // a persistent launch), then the partial outputs and their (m, l) pairs.
+  // a persistent launch), then the partial outputs (in the input dtype) and
+  // their (m, l) pairs.
   size_t workspace_bytes = 0;
   size_t control_bytes = 0;
   int32_t n_cursors = 0;       // n_lists + 1 for a persistent launch, else 0

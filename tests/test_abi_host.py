@@ -239,7 +239,7 @@ def test_read_ceiling_error_codes():
 def test_noalloc_rejects_steps_beyond_its_scratch():
     """The no-allocation verify entry point refuses a step whose partial
     results would not fit its 64 MiB per-device scratch (the full-size probe
-    prefill needs about 272 MiB) before touching the GPU, and checks its
+    prefill needs about 140 MiB) before touching the GPU, and checks its
     pointers like spork_verify_accept."""
     wl = synth.make_prefill(kv=False)
     stp = wl.steps[0]
