@@ -156,8 +156,8 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   }
 
   // Row tiles per workgroup: large row sets are split into near-equal slices
-  // of at most unit_tiles_max tiles; every workgroup of the launch is sized
-  // for the largest slice.
+  // of at most unit_tiles_max tiles (8-wave plans: per range, below); every
+  // workgroup of the launch is sized for the largest slice.
   int32_t row_tiles = 1;
   std::vector<int32_t> range_rows(ranges.size());
   for (size_t r = 0; r < ranges.size(); ++r) {
@@ -169,23 +169,45 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     const int32_t slices = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
     row_tiles = std::max(row_tiles, (tiles + slices - 1) / slices);
   }
-  // 8-wave plans: the slice size (one for the whole plan) that streams the
-  // ranges at the least stage cost, fuller slices first among equals. Near-
-  // equal slices can leave every slice with four tiles on its busiest SIMD
-  // (26 tiles as 13 + 13 cost two full stages per 32 tokens; as 16 + 10,
-  // one full and one three-tile stage).
+  // 8-wave plans slice each range on its own: into the fewest slices of at
+  // most unit_tiles_max tiles (or one more), with the tile counts whose
+  // summed stage weights are least, larger slices first among equals (26
+  // tiles as 16 + 10: a full stage and a three-tile one per 32 tokens, not
+  // 13 + 13, two full ones; 20 tiles as 12 + 8, not 16 + 4).
+  std::vector<std::vector<int32_t>> range_slice_tiles(ranges.size());
   if (shape.persistent && shape.waves == 8) {
-    int64_t best = INT64_MAX;
-    for (int32_t rt = shape.unit_tiles_max; rt >= 1; --rt) {
-      int64_t cost = 0;
-      for (size_t r = 0; r < ranges.size(); ++r) {
-        const int64_t len = ranges[r].hi - ranges[r].lo;
-        for (int32_t done = 0; done < range_rows[r]; done += rt * 16)
-          cost += len * stage_weight8((std::min(rt * 16, range_rows[r] - done) + 15) / 16);
-      }
-      if (cost < best) {
-        best = cost;
-        row_tiles = rt;
+    row_tiles = 1;
+    for (size_t r = 0; r < ranges.size(); ++r) {
+      const int32_t tiles = (range_rows[r] + 15) / 16;
+      const int32_t s0 = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
+      const int32_t max_class = (shape.unit_tiles_max + 3) / 4;  // a slice's busiest-SIMD tiles
+      int64_t best = INT64_MAX;
+      std::vector<int32_t> best_cls, cls;
+      // classes c_1 >= c_2 >= ... (slice i holds up to 4 c_i tiles)
+      std::function<void(int32_t, int32_t, int64_t, int32_t)> search = [&](int32_t left, int32_t top, int64_t cost,
+                                                                           int32_t cap) {
+        if (left == 0) {
+          if (cap >= tiles && cost < best) {
+            best = cost;
+            best_cls = cls;
+          }
+          return;
+        }
+        for (int32_t c = top; c >= 1; --c) {
+          cls.push_back(c);
+          search(left - 1, c, cost + kStageWeight8[c], cap + 4 * c);
+          cls.pop_back();
+        }
+      };
+      for (int32_t sl = s0; sl <= std::min(s0 + 1, tiles); ++sl) search(sl, max_class, 0, 0);
+      std::vector<int32_t>& st = range_slice_tiles[r];
+      int32_t done = 0;
+      for (size_t i = 0; i < best_cls.size(); ++i) {
+        const int32_t rest = static_cast<int32_t>(best_cls.size() - i - 1);  // slices still to fill, one tile each at least
+        const int32_t n = std::min({4 * best_cls[i], shape.unit_tiles_max, tiles - done - rest});
+        st.push_back(n);
+        done += n;
+        row_tiles = std::max(row_tiles, n);
       }
     }
   }
@@ -200,6 +222,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   std::vector<ItemDesc> items;
   std::vector<RowDesc> rows;
   std::vector<Range*> item_range;
+  std::vector<int32_t> item_rng;  // index of the item's range
   p.seqs.assign(seqs, seqs + n_threads);
   p.len = len;
   p.thread_items.assign(n_threads, {});
@@ -236,6 +259,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
             rows.push_back({(row_base[t] + q) * hq + h * gq + j, len[t] - n_rows[t] + q});
       items.push_back(it);
       item_range.push_back(&rg);
+      item_rng.push_back(static_cast<int32_t>(r));
     }
   }
   p.n_items = static_cast<int32_t>(items.size());
@@ -244,7 +268,10 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
   const int32_t per_cu = 2 * row_tiles <= shape.unit_tiles_max ? shape.units_per_cu_half : shape.units_per_cu;
   const int64_t n_wg = static_cast<int64_t>(n_cu) * std::max(1, per_cu);
   std::vector<int32_t> slices_of(items.size());
-  for (size_t it = 0; it < items.size(); ++it) slices_of[it] = (items[it].n_rows + slice_rows - 1) / slice_rows;
+  const bool own_slices = shape.persistent && shape.waves == 8;  // per-range slice tiles (above)
+  for (size_t it = 0; it < items.size(); ++it)
+    slices_of[it] = own_slices ? static_cast<int32_t>(range_slice_tiles[item_rng[it]].size())
+                               : (items[it].n_rows + slice_rows - 1) / slice_rows;
   std::vector<WaveDesc> waves;
   std::vector<int32_t> wg_off;
   auto desc = [&](int32_t item, int32_t lo, int32_t hi, int32_t s) {
@@ -252,8 +279,16 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     w.item = item;
     w.tok_lo = lo;
     w.tok_hi = hi;
-    w.row0 = s * slice_rows;
-    w.nrows = std::min(slice_rows, items[item].n_rows - s * slice_rows);
+    if (own_slices) {
+      const std::vector<int32_t>& st = range_slice_tiles[item_rng[item]];
+      int32_t t0 = 0;
+      for (int32_t j = 0; j < s; ++j) t0 += st[j];
+      w.row0 = 16 * t0;
+      w.nrows = std::min(16 * st[s], items[item].n_rows - w.row0);
+    } else {
+      w.row0 = s * slice_rows;
+      w.nrows = std::min(slice_rows, items[item].n_rows - s * slice_rows);
+    }
     return w;
   };
   if (shape.persistent) {
@@ -293,7 +328,7 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
       }
       tok_cost[it] = 0;
       for (int32_t sl = 0; sl < slices_of[it]; ++sl)
-        tok_cost[it] += stage_weight8((std::min(slice_rows, items[it].n_rows - sl * slice_rows) + 15) / 16);
+        tok_cost[it] += stage_weight8((desc(static_cast<int32_t>(it), 0, 0, sl).nrows + 15) / 16);
     }
     const int64_t per_list = per_cu == 2 ? 2 : 1;
     const int64_t lanes = n_wg / per_list;

@@ -3,6 +3,7 @@ oracle (bit-exact tables, slots, copies, refcounts and free queue), error
 codes, and planner invariants."""
 import copy
 import ctypes
+import functools
 import os
 import re
 
@@ -700,3 +701,49 @@ def test_eight_wave_slices_by_stage_cost():
         assert set(int(x) for x in units[:, 3]) == ({0, 256} if case == "verify-k50" else {0})
         spork.spork_plan_destroy(p)
         spork.spork_cache_destroy(c)
+
+
+def test_eight_wave_slices_each_range_at_least_stage_cost():
+    """8-wave plans slice each range on its own. On the probe prefill (9-51
+    row tiles per range) every item's slices are checked against brute force:
+    the fewest slices (or one more) of at most 16 tiles, and no split into
+    that many slices has a smaller summed stage weight (the weight of a slice
+    by the tiles on its busiest SIMD: 572, 722, 821, 1024 per 1,024)."""
+    weight = {1: 572, 2: 722, 3: 821, 4: 1024}
+    w = lambda t: weight[(t + 3) // 4]
+
+    @functools.lru_cache(maxsize=None)
+    def best(tiles, n):  # least summed weight of n slices of 1..16 tiles adding up to tiles
+        if n == 0:
+            return 0 if tiles == 0 else None
+        out = None
+        for t in range(1, min(16, tiles - n + 1) + 1):
+            rest = best(tiles - t, n - 1)
+            if rest is not None and (out is None or w(t) + rest < out):
+                out = w(t) + rest
+        return out
+
+    wl = _full_size("prefill")
+    c, p = _plan_for(wl)
+    info, img = _decode_image(p)
+    assert info["attn_waves"] == 8
+    units = img.view(np.int32)[: info["n_units"] * 6].reshape(-1, 6)
+    slices = {}
+    for it, _lo, _hi, row0, nrows, _part in units:
+        slices.setdefault(int(it), set()).add((int(row0), int(nrows)))
+    seen = set()
+    for it, sl in slices.items():
+        sl = sorted(sl)
+        rows = sl[-1][0] + sl[-1][1]
+        assert [r0 for r0, _ in sl] == [0] + [r0 + n for r0, n in sl[:-1]]  # contiguous, from row 0
+        tiles = [(n + 15) // 16 for _, n in sl]
+        total = (rows + 15) // 16
+        assert sum(tiles) == total and max(tiles) <= 16
+        s0 = -(-total // 16)
+        assert len(tiles) in (s0, s0 + 1)
+        got = sum(w(t) for t in tiles)
+        assert got == min(x for x in (best(total, s0), best(total, s0 + 1)) if x is not None), (total, tiles)
+        seen.add(len(tiles))
+    assert seen >= {1, 2, 3}, seen   # the workload spans one to four slices per range
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
