@@ -3,7 +3,6 @@
 #include <algorithm>
 #include <climits>
 #include <cstring>
-#include <functional>
 #include <map>
 #include <queue>
 
@@ -180,26 +179,31 @@ std::string build_plan(const BlockManager& bm, const PlanShape& shape, const int
     for (size_t r = 0; r < ranges.size(); ++r) {
       const int32_t tiles = (range_rows[r] + 15) / 16;
       const int32_t s0 = (tiles + shape.unit_tiles_max - 1) / shape.unit_tiles_max;
-      const int32_t max_class = (shape.unit_tiles_max + 3) / 4;  // a slice's busiest-SIMD tiles
+      // A slice of class c (1..4) holds up to 4c tiles, c on its busiest
+      // SIMD. For s0 and s0 + 1 slices, the counts of slices per class with
+      // enough tiles and the least summed weight, more slices of the larger
+      // classes first among equals; past 64 slices, full slices.
+      const int32_t max_class = std::min(4, (shape.unit_tiles_max + 3) / 4);
       int64_t best = INT64_MAX;
-      std::vector<int32_t> best_cls, cls;
-      // classes c_1 >= c_2 >= ... (slice i holds up to 4 c_i tiles)
-      std::function<void(int32_t, int32_t, int64_t, int32_t)> search = [&](int32_t left, int32_t top, int64_t cost,
-                                                                           int32_t cap) {
-        if (left == 0) {
-          if (cap >= tiles && cost < best) {
-            best = cost;
-            best_cls = cls;
-          }
-          return;
-        }
-        for (int32_t c = top; c >= 1; --c) {
-          cls.push_back(c);
-          search(left - 1, c, cost + kStageWeight8[c], cap + 4 * c);
-          cls.pop_back();
-        }
-      };
-      for (int32_t sl = s0; sl <= std::min(s0 + 1, tiles); ++sl) search(sl, max_class, 0, 0);
+      std::vector<int32_t> best_cls;
+      for (int32_t sl = s0; sl <= std::min(s0 + 1, tiles) && sl <= 64; ++sl) {
+        for (int32_t n4 = max_class >= 4 ? sl : 0; n4 >= 0; --n4)
+          for (int32_t n3 = (max_class >= 3 ? sl - n4 : 0); n3 >= 0; --n3)
+            for (int32_t n2 = (max_class >= 2 ? sl - n4 - n3 : 0); n2 >= 0; --n2) {
+              const int32_t n1 = sl - n4 - n3 - n2;
+              if (4 * (4 * n4 + 3 * n3 + 2 * n2 + n1) < tiles) continue;
+              const int64_t cost = n4 * kStageWeight8[4] + n3 * kStageWeight8[3] + n2 * kStageWeight8[2] +
+                                   n1 * kStageWeight8[1];
+              if (cost < best) {
+                best = cost;
+                best_cls.assign(n4, 4);
+                best_cls.insert(best_cls.end(), n3, 3);
+                best_cls.insert(best_cls.end(), n2, 2);
+                best_cls.insert(best_cls.end(), n1, 1);
+              }
+            }
+      }
+      if (best_cls.empty()) best_cls.assign(s0, max_class);  // slices of unit_tiles_max tiles, the last shorter
       std::vector<int32_t>& st = range_slice_tiles[r];
       int32_t done = 0;
       for (size_t i = 0; i < best_cls.size(); ++i) {

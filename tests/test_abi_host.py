@@ -573,6 +573,23 @@ def test_probe_prefill_plan(shape):
     spork.spork_cache_destroy(c)
 
 
+def test_probe_prefill_plan_with_very_many_rows():
+    """A shared range read by 70 probes of 40-50 opener rows (over 28,000
+    rows per KV head, more than 64 slices of 16 tiles): planned quickly, in
+    slices of at most 16 tiles, and every row sees every position up to its
+    own once."""
+    import time
+    wl = synth.make_prefill(sessions=1, prefix=600, probes=70, cot=("uniform", 1, 50), opener=(40, 50))
+    t0 = time.perf_counter()
+    c, p = _plan_for(wl, n_cu=8)
+    assert time.perf_counter() - t0 < 5.0
+    info = spork.spork_plan_get_info(p)
+    assert info["attn_waves"] == 8 and info["max_row_tiles"] <= 16
+    _check_cover(wl, c, p)
+    spork.spork_plan_destroy(p)
+    spork.spork_cache_destroy(c)
+
+
 def test_supersession_plan():
     """The step after a probe is freed and a new one forked: the plan's unique
     bytes and coverage hold on the reused blocks."""
