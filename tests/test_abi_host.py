@@ -574,8 +574,8 @@ def test_probe_prefill_plan(shape):
 
 
 def test_probe_prefill_plan_with_very_many_rows():
-    """A shared range read by 70 probes of 40-50 opener rows (over 28,000
-    rows per KV head, more than 64 slices of 16 tiles): planned quickly, in
+    """A shared range read by 70 probes of 40-50 opener rows (over 25,000
+    rows per KV head, about 100 slices of 16 tiles): planned quickly, in
     slices of at most 16 tiles, and every row sees every position up to its
     own once."""
     import time

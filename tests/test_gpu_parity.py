@@ -142,6 +142,16 @@ def test_probe_prefill(dtype, shape, opener):
     dw.close()
 
 
+def test_probe_prefill_very_many_rows():
+    """A shared range read by 70 probes of 40-50 opener rows each: over 25,000
+    rows per KV head, sliced into about 100 slices of 16 row tiles (the
+    planner's fallback past its slice search)."""
+    say("probe prefill, 70 probes")
+    wl = synth.make_prefill(sessions=1, prefix=600, probes=70, cot=("uniform", 1, 50), opener=(40, 50))
+    dw = run_workload(wl, "prefill 70 probes")
+    dw.close()
+
+
 def test_verify_k50():
     """Verify at the paper's draft length (K = 50): 51 causal rows per
     session, accept lengths planted up to K."""
